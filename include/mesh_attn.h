@@ -1,0 +1,200 @@
+/*
+ * mesh_attn.h -- C ABI of the single-GPU tile compute of Mesh-Attention
+ * (arXiv 2512.20968) for AMD Instinct MI355X (gfx950).
+ *
+ * In Mesh-Attention every GPU owns a 2-D tile of the Q-KV interaction matrix:
+ * a list of Q partitions times a list of KV partitions (the footprints
+ * I_g^Q, I_g^KV of Section 3.1).  After the all-gathers of Algorithm 2 the GPU
+ * computes attention for every (Q_u, KV_v) pair of its tile and merges the
+ * partial results with the online-softmax reducer; after those of Algorithm 3
+ * it computes the partial gradients of every pair.  This library is that
+ * per-GPU compute.  The collectives around it are not part of it.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - The sequence of num_partitions * partition_len tokens is split into
+ *    contiguous partitions of partition_len (P) tokens.  Token r of partition
+ *    p has global position p * P + r; the causal rule (Section 3.7) lets a
+ *    query see a key iff key position <= query position.
+ *  - A tile buffer stacks its partitions in the order of its index list: row
+ *    a * P + r of the Q buffer is token r of partition q_idx[a] (the order an
+ *    all-gather over the Q group delivers).  The same holds for the KV side.
+ *  - Q, O, dO, dQ are [nq * P][num_q_heads][head_dim]; K, V, dK, dV are
+ *    [nkv * P][num_kv_heads][head_dim]; LSE is [num_q_heads][rows], float32,
+ *    natural log.  All dense, row-major, no padding.
+ *  - GQA (Section 4.8): query head h reads KV head h / (num_q_heads /
+ *    num_kv_heads).
+ *  - Device pointers must be 16-byte aligned.  Outputs must not alias inputs.
+ *  - The caller owns every buffer, host and device.  The library never
+ *    allocates or frees device memory and never synchronizes the stream; a
+ *    small process-lifetime cache of pinned host copies of work lists is its
+ *    only state (guarded by a mutex).
+ *  - Arguments are validated on the host before anything is enqueued.  On a
+ *    non-OK status nothing was launched and mesh_attn_last_error() describes
+ *    the problem.  Device work runs asynchronously on `stream`; a launch
+ *    failure returns MA_ERR_HIP.
+ */
+#ifndef MESH_ATTN_H
+#define MESH_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MA_OK = 0,
+  MA_ERR_INVALID_ARG = 1,         /* bad size, index, flag or pointer */
+  MA_ERR_UNSUPPORTED = 2,         /* valid request this build does not serve */
+  MA_ERR_WORKSPACE_TOO_SMALL = 3, /* ws_bytes below the *_workspace_size() */
+  MA_ERR_HIP = 4,                 /* HIP runtime error, text in last_error */
+  MA_ERR_CAPACITY = 5             /* caller-provided output array too small */
+} ma_status_t;
+
+typedef enum { MA_BF16 = 0, MA_FP32 = 1 } ma_dtype_t;
+
+/* Block classes of a (Q block, KV block) pair under the causal rule. */
+enum { MA_CLS_EMPTY = 0, MA_CLS_PARTIAL = 1, MA_CLS_FULL = 2 };
+
+typedef struct {
+  int32_t num_partitions; /* n: partitions of the whole sequence, >= 1        */
+  int32_t partition_len;  /* P: tokens per partition, multiple of the blocks  */
+  int32_t num_q_heads;    /* Hq >= 1                                         */
+  int32_t num_kv_heads;   /* Hkv >= 1, divides Hq                            */
+  int32_t head_dim;       /* d: 64 or 128                                    */
+  int32_t causal;         /* 0 or 1                                          */
+  float softmax_scale;    /* s > 0, finite; usually 1/sqrt(d)                */
+} ma_problem_t;
+
+/* ---------------------------------------------------------------------------
+ * Work list (host only, deterministic).
+ *
+ * The tile's Q buffer is cut into Q blocks of bm rows, its KV buffer into KV
+ * blocks of bn rows (both divide P, so no block straddles partitions).  Q
+ * block a*(P/bm)+qb is block qb of list entry a.  A (Q block, KV block) pair is
+ * EMPTY if no (query, key) pair in it is visible under the causal rule
+ * (Section 3.7), FULL if every pair is (always, without a mask), PARTIAL
+ * otherwise.  Fully masked pairs are skipped by the kernels; PARTIAL pairs are
+ * the only ones that evaluate the per-element mask.
+ * ------------------------------------------------------------------------- */
+
+/* Block shape (rows per Q block, rows per KV block) the kernels of `pass`
+ * (0 = forward, 1 = backward) use for `head_dim`; both are 0 for an
+ * unsupported head_dim or pass. */
+void mesh_attn_block_shape(int32_t head_dim, int32_t pass, int32_t* bm,
+                           int32_t* bn);
+
+/* Class of every block pair into cls[(nq*P/bm) * (nkv*P/bn)] (row-major, Q
+ * block major), values MA_CLS_*.  q_idx, kv_idx are host arrays of distinct
+ * partition indices in [0, num_partitions). */
+ma_status_t mesh_attn_classify(const ma_problem_t* prob, const int32_t* q_idx,
+                               int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                               int32_t bm, int32_t bn, uint8_t* cls);
+
+/* Canonical Q-major run list.  For every Q block in buffer order, for every
+ * KV list entry b in list order, the maximal runs of consecutive KV blocks kb
+ * (ascending) of equal class, EMPTY runs dropped.  Each run is five int32
+ * (qblk, b, kb_begin, kb_end exclusive, cls) written to runs[5*i..5*i+4];
+ * qblk_ptr[q] (nq*P/bm + 1 entries) is the first run of Q block q and its last
+ * entry the run count.  cap is the capacity of runs in runs; if it is too
+ * small, *n_runs gets the required count and MA_ERR_CAPACITY is returned.  A
+ * NULL runs with cap 0 queries the count. */
+ma_status_t mesh_attn_worklist(const ma_problem_t* prob, const int32_t* q_idx,
+                               int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                               int32_t bm, int32_t bn, int32_t* qblk_ptr,
+                               int32_t* runs, int64_t cap, int64_t* n_runs);
+
+/* KV-major mirror: the same rule with the sides swapped.  For every KV block
+ * in buffer order, for every Q list entry a, runs of Q blocks
+ * (kvblk, a, qb_begin, qb_end, cls); kvblk_ptr has nkv*P/bn + 1 entries. */
+ma_status_t mesh_attn_worklist_kv_major(const ma_problem_t* prob,
+                                        const int32_t* q_idx, int32_t nq,
+                                        const int32_t* kv_idx, int32_t nkv,
+                                        int32_t bm, int32_t bn,
+                                        int32_t* kvblk_ptr, int32_t* runs,
+                                        int64_t cap, int64_t* n_runs);
+
+/* ---------------------------------------------------------------------------
+ * Forward (Algorithm 2, the per-pair loop; attention as defined in Section
+ * 2.1, partial (O, lse) as in Section 2.2, merged over the tile's KV footprint
+ * with the online-softmax reducer inside the kernel).
+ * ------------------------------------------------------------------------- */
+
+/* Device workspace bytes mesh_attn_tile_fwd needs for this tile. */
+size_t mesh_attn_fwd_workspace_size(const ma_problem_t* prob, int32_t nq,
+                                    int32_t nkv);
+
+/* O and LSE of every Q row of the tile over every key of the tile.
+ *   q       [nq*P][Hq][d] bf16 device;  k, v [nkv*P][Hkv][d] bf16 device.
+ *   o       [nq*P][Hq][d] device, bf16 (o_dtype MA_BF16, the final output) or
+ *           float32 (MA_FP32, a partial to be merged exactly later).
+ *   lse     [Hq][nq*P] float32 device; -inf for a row that sees no key, whose
+ *           O row is then 0.
+ *   ws      device workspace of ws_bytes >= mesh_attn_fwd_workspace_size().
+ * O = sum_j exp(x_j - LSE) v_j with x_j = s <q, k_j> over the visible keys;
+ * LSE = ln sum_j exp(x_j).  bf16 MFMA products, float32 accumulation and
+ * softmax. */
+ma_status_t mesh_attn_tile_fwd(const ma_problem_t* prob, const int32_t* q_idx,
+                               int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                               const void* q, const void* k, const void* v,
+                               void* o, ma_dtype_t o_dtype, float* lse,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Online-softmax reducer (Section 2.2; the reducer of Algorithm 2's
+ * reduce-scatter).  Folds k_parts partial results of the same rows over
+ * disjoint key sets:  M = max_k lse_k,  lse = M + ln sum_k exp(lse_k - M),
+ * O = sum_k exp(lse_k - lse) O_k.  Parts with lse = -inf weigh 0; a row whose
+ * parts are all -inf gets O = 0, lse = -inf.
+ *   o_parts   [k_parts][rows][heads][head_dim] device, in_dtype.
+ *   lse_parts [k_parts][heads][rows] float32 device.
+ *   o_out     [rows][heads][head_dim] device, out_dtype.
+ *   lse_out   [heads][rows] float32 device.
+ * head_dim must be a multiple of 8 (16-byte vectors) and at most 256;
+ * rows >= 0 (0 launches nothing), 1 <= k_parts <= 4096.
+ * ------------------------------------------------------------------------- */
+ma_status_t mesh_attn_lse_merge(int32_t k_parts, int64_t rows, int32_t heads,
+                                int32_t head_dim, const void* o_parts,
+                                ma_dtype_t in_dtype, const float* lse_parts,
+                                void* o_out, ma_dtype_t out_dtype,
+                                float* lse_out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Backward (Algorithm 3, the per-pair loop, summed over the tile).
+ * ------------------------------------------------------------------------- */
+
+/* Device workspace bytes mesh_attn_tile_bwd needs for this tile. */
+size_t mesh_attn_bwd_workspace_size(const ma_problem_t* prob, int32_t nq,
+                                    int32_t nkv);
+
+/* Gradients of <dO, O> for the tile, given the FINAL O and LSE of its Q rows
+ * (those of the full key set, as gathered in Algorithm 3).
+ *   q, o, d_o  [nq*P][Hq][d] bf16 device;  k, v [nkv*P][Hkv][d] bf16 device.
+ *   lse        [Hq][nq*P] float32 device.
+ *   dq         [nq*P][Hq][d] float32 device;  dk, dv [nkv*P][Hkv][d] float32.
+ *   accumulate 0: overwrite dq, dk, dv;  1: add into them.
+ * With P_ij = exp(s <q_i,k_j> - LSE_i) over visible pairs, D_i = <dO_i, O_i>:
+ * dV_j = sum_i P_ij dO_i;  dS_ij = P_ij (<dO_i, v_j> - D_i);
+ * dQ_i = s sum_j dS_ij k_j;  dK_j = s sum_i dS_ij q_i.  Under GQA dK, dV of a
+ * KV head sum over its query heads.  Deterministic (no atomics). */
+ma_status_t mesh_attn_tile_bwd(const ma_problem_t* prob, const int32_t* q_idx,
+                               int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                               const void* q, const void* k, const void* v,
+                               const void* o, const void* d_o,
+                               const float* lse, float* dq, float* dk,
+                               float* dv, int32_t accumulate, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/* Text of the last non-OK status returned on the calling thread ("" if none).
+ * The pointer stays valid until the next library call on that thread. */
+const char* mesh_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MESH_ATTN_H */

@@ -1,0 +1,89 @@
+// Internal interface between the host library (host.cpp) and the HIP kernel
+// translation units.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mesh_attn {
+
+// gfx950 (MI355X) has 8 XCDs; consecutive workgroup ids are dispatched to
+// XCDs round robin, so id i runs on XCD i % 8.
+constexpr int kNumXcd = 8;
+
+// Forward block shape: 4 waves x 32 query rows, 64 keys per LDS stage.
+constexpr int kFwdBM = 128;
+constexpr int kFwdBN = 64;
+
+// Backward block shapes.
+constexpr int kBwdBM = 128;  // Q rows per dQ workgroup (4 waves x 32)
+constexpr int kBwdBN = 128;  // KV rows per dK/dV workgroup (4 waves x 32)
+
+// One run of consecutive KV blocks of one KV list entry, as the kernels read
+// it: x = first KV block (index into the tile's KV buffer, in blocks of the
+// pass's KV block size), y = number of blocks, z = class (MA_CLS_*),
+// w = position of the Q block's first row minus position of the run's first
+// key (the causal mask of a PARTIAL run: key j of the run is hidden from
+// query i of the block iff j - i > w).
+struct DevRun {
+  int32_t blk0, nblk, cls, delta;
+};
+
+struct FwdParams {
+  const uint16_t* q;   // bf16 [rows_q][hq][d]
+  const uint16_t* k;   // bf16 [rows_kv][hkv][d]
+  const uint16_t* v;
+  void* o;             // bf16 or f32 [rows_q][hq][d]
+  float* lse;          // [hq][rows_q]
+  const int32_t* qblk_ptr;   // [n_qblk + 1]
+  const DevRun* runs;
+  const int2* order;         // [grid] (qblk, q head); qblk < 0: idle slot
+  int64_t rows_q;
+  int32_t hq, hkv, group;
+  float scale_log2;    // softmax scale * log2(e)
+};
+
+hipError_t launch_tile_fwd(const FwdParams& p, int head_dim, bool out_f32,
+                           int grid, hipStream_t stream);
+
+struct MergeParams {
+  const void* o_parts;
+  const float* lse_parts;
+  void* o_out;
+  float* lse_out;
+  int64_t rows;
+  int32_t k_parts, heads, head_dim;
+};
+
+hipError_t launch_lse_merge(const MergeParams& p, bool in_f32, bool out_f32,
+                            hipStream_t stream);
+
+struct BwdParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint16_t* o;
+  const uint16_t* d_o;
+  const float* lse;
+  float* dq;
+  float* dk;
+  float* dv;
+  float* delta;        // workspace [hq][rows_q]: rowsum(dO * O)
+  // Q-major runs (dQ kernel): Q blocks of kBwdBM rows, KV blocks of kBwdBN.
+  const int32_t* qblk_ptr;
+  const DevRun* qruns;
+  const int2* qorder;
+  // KV-major runs (dK/dV kernel): delta field is kv-first minus q-first.
+  const int32_t* kvblk_ptr;
+  const DevRun* kvruns;
+  const int2* kvorder;   // (kvblk, kv head)
+  int64_t rows_q, rows_kv;
+  int32_t hq, hkv, group;
+  float scale, scale_log2;
+  int32_t accumulate;
+};
+
+hipError_t launch_tile_bwd(const BwdParams& p, int head_dim, int grid_q,
+                           int grid_kv, hipStream_t stream);
+
+}  // namespace mesh_attn

@@ -1,0 +1,157 @@
+// Device helpers shared by the tile kernels (gfx950, wave64).
+//
+// MFMA conventions (v_mfma_f32_32x32x16_bf16): lane l of a wave holds, for
+// the A operand, row l % 32 and the 8 k-values of group l / 32; for B,
+// column l % 32 and the same k group; the 16 accumulator registers of lane l
+// hold column l % 32 and rows 8*(r/4) + 4*(l/32) + r%4.
+//
+// Tiles staged in LDS are 64 rows of one head.  A row-major tile is
+// [64][D] bf16 with its 16-byte chunks XOR-swizzled by row; a transposed
+// tile is [D][64] bf16 with chunks swizzled by dim.  Both swizzles make the
+// MFMA operand reads (16 lanes reading 16 consecutive rows at one logical
+// chunk) hit distinct banks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mesh_attn {
+namespace dev {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;  // four waves
+constexpr int kTileRows = 64;  // rows of a staged tile
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b,
+                                         const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float exp2_fast(float x) {
+  return __builtin_amdgcn_exp2f(x);
+}
+
+__device__ __forceinline__ void zero(f32x16& a) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a[i] = 0.f;
+}
+
+// Order in which the 32 rows of an operand tile are fed to the MFMA: bits 2
+// and 3 of the row index swapped.  With it, accumulator register r of lane
+// half h holds row 16*(r/8) + 8*h + r%8, i.e. every lane half owns runs of 8
+// consecutive rows -- the k-contiguous layout the next MFMA's operand needs.
+__device__ __forceinline__ int mfma_row_perm(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+// Row of the permuted 32-row tile held by accumulator register r, lane half h.
+__device__ __forceinline__ int acc_row(int r, int h) {
+  return (r >> 3) * 16 + h * 8 + (r & 7);
+}
+
+template <int D>
+__device__ __forceinline__ int row_chunk(int row, int chunk) {
+  return chunk ^ (D == 128 ? (row & 15) : (row & 7));
+}
+__device__ __forceinline__ int col_chunk(int dim, int chunk) {
+  return chunk ^ ((dim ^ (dim >> 3)) & 7);
+}
+
+// 16-byte A/B operand read from a row-major [64][D] tile: row `row`, dims
+// 16*kk + 8*h .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 read_rows(const uint16_t* t, int row, int kk,
+                                            int h) {
+  return *reinterpret_cast<const bf16x8*>(
+      t + row * D + row_chunk<D>(row, 2 * kk + h) * 8);
+}
+
+// 16-byte operand read from a transposed [D][64] tile: dim `dim`, rows
+// 16*ss + 8*h .. +7.
+__device__ __forceinline__ bf16x8 read_cols(const uint16_t* t, int dim, int ss,
+                                            int h) {
+  return *reinterpret_cast<const bf16x8*>(
+      t + dim * kTileRows + col_chunk(dim, 2 * ss + h) * 8);
+}
+
+__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
+  return (a & 0xffffu) | (b << 16);
+}
+__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
+  return (a >> 16) | (b & 0xffff0000u);
+}
+
+// 64 rows x D of one head, global -> registers -> LDS.  Thread t owns the
+// 16-byte chunk t % (D/8) of NLD consecutive rows, so a wave's loads cover
+// whole 2*D-byte row segments (coalesced) and the transposed store needs only
+// an in-register NLD x 8 transpose.
+template <int D>
+struct RowTile {
+  static constexpr int CPR = D / 8;
+  static constexpr int NLD = kTileRows * CPR / kThreads;  // 4 (D=128), 2 (64)
+  static_assert(NLD == 2 || NLD == 4, "unsupported head_dim");
+  u32x4 r[NLD];
+
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ g,
+                                       int64_t row0, int heads, int head,
+                                       int tid) {
+    const int c = tid % CPR;
+    const int64_t rb = row0 + (tid / CPR) * NLD;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      r[j] = *reinterpret_cast<const u32x4*>(
+          g + ((rb + j) * heads + head) * D + c * 8);
+  }
+
+  __device__ __forceinline__ void store_rows(uint16_t* t, int tid) const {
+    const int c = tid % CPR;
+    const int rb = (tid / CPR) * NLD;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+      *reinterpret_cast<u32x4*>(t + (rb + j) * D + row_chunk<D>(rb + j, c) * 8) =
+          r[j];
+  }
+
+  __device__ __forceinline__ void store_cols(uint16_t* t, int tid) const {
+    const int c = tid % CPR;
+    const int rb = (tid / CPR) * NLD;
+    const int chunk = rb >> 3, sub = rb & 7;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int dim = c * 8 + e;
+      const int w = e >> 1;
+      uint16_t* p = t + dim * kTileRows + col_chunk(dim, chunk) * 8 + sub;
+      if constexpr (NLD == 4) {
+        u32x2 val;
+        val[0] = (e & 1) ? pack_hi(r[0][w], r[1][w]) : pack_lo(r[0][w], r[1][w]);
+        val[1] = (e & 1) ? pack_hi(r[2][w], r[3][w]) : pack_lo(r[2][w], r[3][w]);
+        *reinterpret_cast<u32x2*>(p) = val;
+      } else {
+        *reinterpret_cast<uint32_t*>(p) =
+            (e & 1) ? pack_hi(r[0][w], r[1][w]) : pack_lo(r[0][w], r[1][w]);
+      }
+    }
+  }
+};
+
+// Operand fragments of 32 rows held in registers for a whole workgroup
+// item: lane (l % 32, half h) holds row l % 32, dims 16*kk + 8*h .. +7.
+template <int D>
+__device__ __forceinline__ void load_frags(bf16x8 (&f)[D / 16],
+                                           const uint16_t* __restrict__ g,
+                                           int64_t row, int heads, int head,
+                                           int h) {
+  const uint16_t* p = g + (row * heads + head) * D + h * 8;
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk)
+    f[kk] = *reinterpret_cast<const bf16x8*>(p + kk * 16);
+}
+
+}  // namespace dev
+}  // namespace mesh_attn

@@ -1,0 +1,196 @@
+"""GPU parity of mesh_attn_tile_fwd and mesh_attn_lse_merge against the
+float64 oracle, through the C ABI, on the same seeded inputs."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_20968_amd as ma
+from mesh_inputs import CONFIGS, make_merge_parts, make_qkv, sample_rows
+
+from helpers import check_fwd, log, run_fwd, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(cfg, dev):
+    q, k, v, extra = make_qkv(cfg)
+    return (q, k, v), tuple(t.to(dev) for t in (q, k, v)), extra
+
+
+def _problem(cfg, **kw):
+    p = cfg.problem()
+    p.update(kw)
+    return p
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_config1_full_tile_fused_and_split_merge(gpu, causal):
+    """Tiny tile {0,1} x {0,1}: every row checked, by the fused call and by one
+    call per KV partition (float32 partials) folded by the merge kernel."""
+    cfg = CONFIGS[1]
+    prob = _problem(cfg, causal=causal)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    P = cfg.partition_len
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, to_np(q),
+                                 to_np(k), to_np(v))
+    check_fwd(f"cfg1 causal={causal} fused", to_np(o), to_np(lse), ro, rl)
+    parts = [run_fwd(prob, cfg.q_idx, [cfg.kv_idx[b]],
+                     qd, kd[b * P:(b + 1) * P].contiguous(),
+                     vd[b * P:(b + 1) * P].contiguous(), torch.float32)
+             for b in range(cfg.nkv)]
+    po = torch.stack([p[0] for p in parts])
+    pl = torch.stack([p[1] for p in parts])
+    mo = torch.empty_like(o)
+    ml = torch.empty_like(lse)
+    ma.mesh_attn_lse_merge(po, pl, mo, ml)
+    torch.cuda.synchronize()
+    check_fwd(f"cfg1 causal={causal} split+merge", to_np(mo), to_np(ml), ro, rl)
+    # Each float32 partial is itself a tile result over one KV partition.
+    for b in range(cfg.nkv):
+        rpo, rpl = oracle.tile_forward(prob, cfg.q_idx, [cfg.kv_idx[b]],
+                                       to_np(q), to_np(k[b * P:(b + 1) * P]),
+                                       to_np(v[b * P:(b + 1) * P]))
+        check_fwd(f"cfg1 causal={causal} partial {b}", to_np(po[b]),
+                  to_np(pl[b]), rpo, rpl)
+
+
+def test_config1_convex_combination(gpu):
+    """Every output row is a convex combination of V rows: per channel it lies
+    within [min_j v_j, max_j v_j] over the visible keys (up to bf16 rounding of
+    the output)."""
+    cfg = CONFIGS[1]
+    prob = _problem(cfg, causal=1)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, torch.float32)
+    torch.cuda.synchronize()
+    og = to_np(o)
+    vn = to_np(v)
+    P = cfg.partition_len
+    qpos = oracle.token_positions(cfg.q_idx, P)
+    kpos = oracle.token_positions(cfg.kv_idx, P)
+    for h in range(cfg.num_q_heads):
+        for i in range(0, og.shape[0], 7):
+            vis = kpos <= qpos[i]
+            lo = vn[vis, h].min(axis=0)
+            hi = vn[vis, h].max(axis=0)
+            assert np.all(og[i, h] >= lo - 1e-5) and np.all(og[i, h] <= hi + 1e-5)
+
+
+def _sampled_parity(cfg, gpu, rows_extra=None, heads=None):
+    (q, k, v), (qd, kd, vd), extra = _inputs(cfg, gpu)
+    prob = cfg.problem()
+    log(f"{cfg.name}: launching forward")
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    extra_local = extra.get("q_outlier_rows", ())
+    rows = sample_rows(cfg, cfg.nq, extra_local=extra_local)
+    heads = list(range(cfg.num_q_heads)) if heads is None else heads
+    log(f"{cfg.name}: oracle on {len(rows)} rows x {len(heads)} heads")
+    ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, q.float().numpy(),
+                                 k.float().numpy(), v.float().numpy(),
+                                 rows=rows, heads=heads)
+    og = o[torch.tensor(rows, device=gpu)][:, heads].float().cpu().numpy()
+    lg = lse[heads][:, torch.tensor(rows, device=gpu)].cpu().numpy()
+    check_fwd(f"{cfg.name} sampled", og, lg, ro, rl)
+    return o, lse
+
+
+def test_config2_causal_64k(gpu):
+    _sampled_parity(CONFIGS[2], gpu)
+
+
+def test_config3_mesh1m_noncausal_gqa(gpu):
+    _sampled_parity(CONFIGS[3], gpu)
+
+
+def test_config4_mesh1m_causal_outliers(gpu):
+    _sampled_parity(CONFIGS[4], gpu)
+
+
+def test_tile_above_diagonal_has_no_visible_key(gpu):
+    """Causal tile whose KV partitions all lie after its Q partitions: every
+    row sees nothing, O = 0 and LSE = -inf.  A mixed tile keeps both kinds."""
+    cfg = dataclasses.replace(CONFIGS[1], q_idx=[0, 1], kv_idx=[2, 3], seed=5)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    prob = _problem(cfg, causal=1)
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    assert torch.all(o == 0) and torch.all(torch.isneginf(lse))
+    cfg2 = dataclasses.replace(CONFIGS[1], q_idx=[0, 3], kv_idx=[2, 1], seed=6)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg2, gpu)
+    o, lse = run_fwd(prob, cfg2.q_idx, cfg2.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    ro, rl = oracle.tile_forward(prob, cfg2.q_idx, cfg2.kv_idx, to_np(q),
+                                 to_np(k), to_np(v))
+    assert np.isneginf(rl).any() and np.isfinite(rl).any()
+    check_fwd("mixed empty rows", to_np(o), to_np(lse), ro, rl)
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(128, 8, 2), (64, 6, 3), (128, 4, 4)])
+def test_kvr_strided_list_gqa_causal(gpu, d, hq, hkv):
+    """Strided, non-contiguous KV footprint as KV Partition Rotation produces
+    (c + t*a), several Q partitions spanning the diagonal, GQA, both head dims;
+    every row checked."""
+    cfg = dataclasses.replace(CONFIGS[1], num_partitions=9, partition_len=256,
+                              q_idx=[3, 4, 5], kv_idx=[1, 4, 7],
+                              num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                              causal=True, seed=9)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    prob = cfg.problem()
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, to_np(q),
+                                 to_np(k), to_np(v))
+    check_fwd(f"kvr d={d} hq={hq} hkv={hkv}", to_np(o), to_np(lse), ro, rl)
+
+
+def test_forward_is_deterministic(gpu):
+    cfg = dataclasses.replace(CONFIGS[2], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
+                              partition_len=1024, num_q_heads=8,
+                              num_kv_heads=8)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    prob = cfg.problem()
+    o1, l1 = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    o2, l2 = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+@pytest.mark.parametrize("kparts,rows,heads,d,in_dt,out_dt,ninf", [
+    (1, 37, 3, 64, torch.float32, torch.float32, 0.0),
+    (2, 1000, 4, 64, torch.float32, torch.bfloat16, 0.1),
+    (5, 777, 2, 128, torch.bfloat16, torch.bfloat16, 0.3),
+    (16, 4096, 4, 128, torch.bfloat16, torch.float32, 0.0),
+    (9, 333, 1, 8, torch.float32, torch.float32, 0.5),
+])
+def test_merge_parity(gpu, kparts, rows, heads, d, in_dt, out_dt, ninf):
+    o, lse = make_merge_parts(kparts, rows, heads, d, seed=kparts + rows,
+                              dtype=in_dt, neg_inf_frac=ninf)
+    if ninf > 0:
+        lse[:, 0, :3] = float("-inf")   # rows with every part empty
+    od, ld = o.to(gpu), lse.to(gpu)
+    mo = torch.empty((rows, heads, d), dtype=out_dt, device=gpu)
+    ml = torch.empty((heads, rows), dtype=torch.float32, device=gpu)
+    ma.mesh_attn_lse_merge(od, ld, mo, ml)
+    torch.cuda.synchronize()
+    on = o.float().numpy()
+    ln = lse.numpy()
+    for h in range(heads):
+        ro, rl = oracle.lse_merge(on[:, :, h], ln[:, h])
+        check_fwd(f"merge k={kparts} h={h}", to_np(mo[:, h])[:, None],
+                  to_np(ml[h])[None], ro[:, None], rl[None])
+
+
+def test_merge_zero_rows_is_noop(gpu):
+    o = torch.empty((3, 0, 2, 64), dtype=torch.bfloat16, device=gpu)
+    lse = torch.empty((3, 2, 0), dtype=torch.float32, device=gpu)
+    mo = torch.empty((0, 2, 64), dtype=torch.bfloat16, device=gpu)
+    ml = torch.empty((2, 0), dtype=torch.float32, device=gpu)
+    ma.mesh_attn_lse_merge(o, lse, mo, ml)
+    torch.cuda.synchronize()
