@@ -1,0 +1,133 @@
+"""GPU parity of mesh_attn_tile_bwd against the float64 oracle, through the C
+ABI.  The GPU backward consumes the GPU forward's O (bf16) and LSE, as a
+caller would; the oracle recomputes its own float64 forward."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_20968_amd as ma
+from mesh_inputs import CONFIGS, make_grad, make_qkv, sample_rows
+
+from helpers import check_grad, log, run_fwd, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse, accumulate=0, init=None):
+    P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
+                     cfg.head_dim)
+    dev = qd.device
+    if init is None:
+        dq = torch.empty((cfg.nq * P, hq, d), dtype=torch.float32, device=dev)
+        dk = torch.empty((cfg.nkv * P, hkv, d), dtype=torch.float32,
+                         device=dev)
+        dv = torch.empty_like(dk)
+    else:
+        dq, dk, dv = (t.clone() for t in init)
+    ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o, dod, lse,
+                          dq, dk, dv, accumulate=accumulate)
+    return dq, dk, dv
+
+
+def _setup(cfg, gpu):
+    q, k, v, _ = make_qkv(cfg)
+    do = make_grad(cfg)
+    qd, kd, vd, dod = (t.to(gpu) for t in (q, k, v, do))
+    prob = cfg.problem()
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    return prob, (q, k, v, do), (qd, kd, vd, dod), o, lse
+
+
+SMALL = [
+    # (q_idx, kv_idx, hq, hkv, d, causal)
+    ([0, 1], [0, 1], 4, 4, 64, False),
+    ([0, 1], [0, 1], 4, 4, 64, True),
+    ([2, 3], [0, 1, 2, 3], 4, 2, 128, True),
+    ([3, 1], [1, 0, 3], 6, 3, 128, True),
+    ([1, 2], [0, 3], 2, 1, 128, False),
+]
+
+
+@pytest.mark.parametrize("q_idx,kv_idx,hq,hkv,d,causal", SMALL)
+def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
+    """Small tiles (GQA, both head dims, causal and not, permuted lists):
+    every row of dQ, dK, dV checked."""
+    cfg = dataclasses.replace(CONFIGS[1], num_partitions=4, partition_len=256,
+                              q_idx=q_idx, kv_idx=kv_idx, num_q_heads=hq,
+                              num_kv_heads=hkv, head_dim=d, causal=causal,
+                              seed=21, grad_seed=22)
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    torch.cuda.synchronize()
+    rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
+        prob, q_idx, kv_idx, to_np(q), to_np(k), to_np(v), to_np(do))
+    tag = f"tile {q_idx}x{kv_idx} hq={hq} hkv={hkv} d={d} c={causal}"
+    check_grad(f"{tag} dq", to_np(dq), rdq)
+    check_grad(f"{tag} dk", to_np(dk), rdk)
+    check_grad(f"{tag} dv", to_np(dv), rdv)
+
+
+def test_accumulate_adds_into_outputs(gpu):
+    cfg = dataclasses.replace(CONFIGS[1], causal=True, seed=31, grad_seed=32)
+    prob, _, (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    g1 = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    init = tuple(torch.randn_like(t) for t in g1)
+    g2 = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse, accumulate=1, init=init)
+    torch.cuda.synchronize()
+    for a, b, c in zip(g1, g2, init):
+        torch.testing.assert_close(b, a + c, rtol=0, atol=1e-5)
+
+
+def test_backward_is_deterministic(gpu):
+    cfg = dataclasses.replace(CONFIGS[2], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
+                              partition_len=1024, num_q_heads=8,
+                              num_kv_heads=8, grad_seed=4)
+    prob, _, (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    a = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    b = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_config5_backward_causal_64k(gpu):
+    """Full-size backward of the causal 64K tile.  The oracle runs its own
+    float64 forward for every row of three heads, then checks dQ on the
+    sampled Q rows and dK, dV on sampled KV rows of those heads.  On all
+    heads, two identities that hold because the tile holds every key the Q
+    rows can see: sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
+    cfg = CONFIGS[5]
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    log("config 5: GPU backward")
+    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    torch.cuda.synchronize()
+    # Identities, all heads.  P and dS are rounded to bf16 before the MFMAs
+    # (relative error 2^-9 per term, random-walking over ~10^4 terms), so the
+    # sums are compared with the L1 mass of the terms they add up.
+    sdk = dk.sum(0)
+    sdv = dv.sum(0)
+    sdo = dod.float().sum(0)
+    mass_k = dk.abs().sum(0)
+    mass_v = dv.abs().sum(0)
+    rk = float((sdk.abs() / mass_k).max())
+    rv = float(((sdv - sdo).abs() / mass_v).max())
+    log(f"config 5: max |sum dK| / sum|dK| = {rk:.3e}, "
+        f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
+    assert rk <= 1e-2 and rv <= 1e-2
+    heads = [0, 17, 31]
+    q_rows = sample_rows(cfg, cfg.nq)
+    kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000)
+    log(f"config 5: oracle on heads {heads}, {len(q_rows)} dQ rows, "
+        f"{len(kv_rows)} dK/dV rows")
+    rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
+        prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do),
+        kv_heads=heads, q_rows=q_rows, kv_rows=kv_rows)
+    qr = torch.tensor(q_rows, device=gpu)
+    kr = torch.tensor(kv_rows, device=gpu)
+    check_grad("config 5 dq", to_np(dq[qr][:, q_heads]), rdq)
+    check_grad("config 5 dk", to_np(dk[kr][:, heads]), rdk)
+    check_grad("config 5 dv", to_np(dv[kr][:, heads]), rdv)
