@@ -124,9 +124,16 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--legs", default="fwd,merge,bwd")
+    ap.add_argument("--workload", type=int, default=2, choices=(2, 3, 4),
+                    help="forward tile: 2 causal 64K (default), 3 1M-token "
+                         "non-causal GQA 16x16 tile, 4 1M-token causal 16x16 "
+                         "tile with outliers (backward always runs on 2)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one 1 GiB device-to-device copy (HBM "
+                         "counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for "
@@ -141,7 +148,9 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg = CONFIGS[2]
+    cfg = CONFIGS[args.workload]
+    if "bwd" in legs and args.workload != 2:
+        legs.remove("bwd")
     prob = cfg.problem()
     P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
                      cfg.head_dim)
@@ -186,6 +195,16 @@ def main():
             ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o,
                                   do, lse, dq, dk, dv, ws=ws_b)
             if ev: ev["bwd"][1].record(stream)
+
+    if args.calib_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration copy: 1073741824 bytes read, 1073741824 written")
+        del src, dst
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):

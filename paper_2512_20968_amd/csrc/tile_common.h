@@ -153,5 +153,46 @@ __device__ __forceinline__ void load_frags(bf16x8 (&f)[D / 16],
     f[kk] = *reinterpret_cast<const bf16x8*>(p + kk * 16);
 }
 
+// ---------------------------------------------------------------------------
+// Raw buffer loads: the 128-bit descriptor holds a scalar base address and a
+// byte range; the per-lane offset is a 32-bit VGPR and the per-load offset a
+// scalar, so loads of a tile need no per-load vector address arithmetic, and
+// reads past the range return zero instead of touching memory.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  // Word 3 = 0x00020000: 32-bit data format, the gfx9-family setting.
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buffer_load16(rsrc_t r, uint32_t voff,
+                                               uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(voff),
+                                               static_cast<int>(soff), 0);
+}
+
+// ---------------------------------------------------------------------------
+// LDS transpose read (gfx950 ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane s supplies the address of 4 consecutive bf16 values x[s][0..3];
+// lane l receives x[4e + l/4][l%4] as its element e.  With lane s pointing at
+// row (r0 + s/4), columns (c0 + 4*(s%4)) .. +3 of a row-major tile, lane l
+// receives column c0 + l of rows r0 .. r0+3: a transposed 4x16 block.
+// ---------------------------------------------------------------------------
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ s16x4 lds_read_tr16(const void* lds_addr) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(lds_addr));
+}
+
+__device__ __forceinline__ bf16x8 join_bf16(const s16x4& lo, const s16x4& hi) {
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
 }  // namespace dev
 }  // namespace mesh_attn

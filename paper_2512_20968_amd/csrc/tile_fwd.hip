@@ -8,141 +8,65 @@
 // accumulates P V -- the per-pair computation of Algorithm 2 with the
 // online-softmax reducer applied inside the kernel (Section 2.2).
 //
-// Layout choices (all for 64-wide wavefronts and the 32x32x16 bf16 MFMA):
+// Layout choices (64-wide wavefronts, v_mfma_f32_32x32x16_bf16):
 //  * Scores are computed transposed, S^T = K Q^T (A = K rows from LDS,
 //    B = Q columns held in registers for the whole item), so each lane owns
-//    one query row (lane % 32) and the row max / row sum are in-lane
-//    reductions plus one exchange between the two half-waves.
-//  * The K rows of a 32-key tile are fed to the MFMA in an order that swaps
-//    bits 2 and 3 of the row index.  The S^T accumulator then holds, for lane
-//    half h, keys 8h..8h+7 (+16) in consecutive registers -- exactly the
-//    k-contiguous B operand that O^T += V^T P^T needs, so P goes from the
-//    score accumulator into the PV MFMA with a convert and no shuffles.
-//  * V is staged into LDS transposed ([dim][key]) through a 4x8 register
-//    transpose, so the V^T A operand is one 16-byte LDS read per MFMA.
-//  * K and V^T tiles are double buffered in LDS with XOR-swizzled 16-byte
-//    chunks (conflict-free reads); the next block's global loads (coalesced
-//    16-byte) are issued before the current block's MFMAs.
+//    one query row and the row max / row sum are in-lane reductions plus one
+//    exchange between the two half-waves.
+//  * K rows are fed to the MFMA in an order that swaps bits 2 and 3 of the
+//    row index, which leaves P^T in the accumulators already laid out as the
+//    k-contiguous B operand of O^T += V^T P^T.
+//  * K and V tiles are stored row-major in LDS with padded rows (272 B and
+//    320 B for d = 128), conflict-free for the reads below and affine in the
+//    loop indices, so every LDS read is one base register plus an immediate.
+//  * The V^T operand comes straight from the row-major V tile through the
+//    LDS transpose read (ds_read_b64_tr_b16), two per MFMA.
+//  * Global loads are raw buffer loads: scalar base per KV block, one
+//    per-lane offset register, scalar per-load offsets.  The next block's
+//    loads are issued before the current block's MFMAs; K/V tiles are double
+//    buffered in LDS with one barrier per block.
 //  * Softmax runs in the log2 domain with the scale folded into one FMA
-//    before v_exp_f32.
+//    before v_exp_f32.  The running max is exact (the largest probability of
+//    a row is exactly 1, which keeps its bf16 rounding error-free), but the
+//    O rescale is skipped when no row of the wave has a new max -- a
+//    wave-uniform branch taken on a small fraction of blocks once the max has
+//    settled.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "internal.h"
+#include "tile_common.h"
 
 namespace mesh_attn {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+using namespace dev;
 
 constexpr int BM = kFwdBM;  // 128
 constexpr int BN = kFwdBN;  // 64
-constexpr int NT = 256;     // 4 waves
+constexpr int NT = kThreads;
 
-__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b,
-                                         const f32x16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ float fast_exp2(float x) {
-  return __builtin_amdgcn_exp2f(x);
-}
+template <int D>
+struct FwdLayout {
+  static constexpr int KSTR = 2 * D + 16;   // K tile row stride, bytes
+  static constexpr int VSTR = 2 * D + 64;   // V tile row stride, bytes
+  static constexpr int KBYTES = BN * KSTR;
+  static constexpr int VBYTES = BN * VSTR;
+  static constexpr int STAGE = KBYTES + VBYTES;
+  static constexpr int SMEM = 2 * STAGE;
+  static constexpr int CPR = D / 8;         // 16-byte chunks per row
+  static constexpr int RSTEP = NT / CPR;    // rows per load pass
+  static constexpr int NLD = BN / RSTEP;    // loads per thread per tensor
+};
 
 // Row order of a 32-key tile as fed to the MFMA: swap bits 2 and 3.
-__device__ __forceinline__ int key_perm(int r) {
-  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
-}
-
-// 16-byte chunk swizzles.  K tile: rows of D bf16; V^T tile: rows of BN bf16.
-template <int D>
-__device__ __forceinline__ int k_chunk(int row, int chunk) {
-  return chunk ^ (D == 128 ? (row & 15) : (row & 7));
-}
-__device__ __forceinline__ int vt_chunk(int dim, int chunk) {
-  return chunk ^ ((dim ^ (dim >> 3)) & 7);
-}
-
-__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
-  return (a & 0xffffu) | (b << 16);
-}
-__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
-  return (a >> 16) | (b & 0xffff0000u);
-}
-
-template <int D>
-struct Stage {
-  static constexpr int CPR = D / 8;        // 16-byte chunks per K row
-  static constexpr int RSTEP = NT / CPR;   // K rows covered per load pass
-  static constexpr int NLD = BN / RSTEP;   // loads per thread per tensor
-  u32x4 k[NLD];
-  u32x4 v[NLD];
-
-  // Global -> registers for KV block `blk` (rows blk*BN ..) of KV head hk.
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ kg,
-                                       const uint16_t* __restrict__ vg,
-                                       int64_t blk, int hkv, int hk, int tid) {
-    const int c = tid % CPR;
-    const int r0 = tid / CPR;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int64_t row = blk * BN + r0 + i * RSTEP;
-      k[i] = *reinterpret_cast<const u32x4*>(kg + (row * hkv + hk) * D + c * 8);
-    }
-    // V: this thread takes NLD consecutive keys of one 8-dim slice.
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int64_t row = blk * BN + r0 * NLD + j;
-      v[j] = *reinterpret_cast<const u32x4*>(vg + (row * hkv + hk) * D + c * 8);
-    }
-  }
-
-  // Registers -> LDS: K as [key][dim], V transposed as [dim][key].
-  __device__ __forceinline__ void store(uint16_t* sk, uint16_t* svt, int tid) {
-    const int c = tid % CPR;
-    const int r0 = tid / CPR;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int row = r0 + i * RSTEP;
-      *reinterpret_cast<u32x4*>(sk + row * D + k_chunk<D>(row, c) * 8) = k[i];
-    }
-    const int key0 = r0 * NLD;  // first of this thread's NLD keys
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int dim = c * 8 + e;
-      const int w = e >> 1;
-      uint16_t* rowp = svt + dim * BN;
-      if constexpr (NLD == 4) {
-        u32x2 val;
-        if (e & 1) {
-          val[0] = pack_hi(v[0][w], v[1][w]);
-          val[1] = pack_hi(v[2][w], v[3][w]);
-        } else {
-          val[0] = pack_lo(v[0][w], v[1][w]);
-          val[1] = pack_lo(v[2][w], v[3][w]);
-        }
-        const int chunk = key0 >> 3, sub = key0 & 7;
-        *reinterpret_cast<u32x2*>(rowp + vt_chunk(dim, chunk) * 8 + sub) = val;
-      } else {
-        static_assert(NLD == 2, "unsupported head_dim");
-        const uint32_t val = (e & 1) ? pack_hi(v[0][w], v[1][w])
-                                     : pack_lo(v[0][w], v[1][w]);
-        const int chunk = key0 >> 3, sub = key0 & 7;
-        *reinterpret_cast<uint32_t*>(rowp + vt_chunk(dim, chunk) * 8 + sub) =
-            val;
-      }
-    }
-  }
-};
+__device__ __forceinline__ int key_perm(int r) { return mfma_row_perm(r); }
 
 template <int D, bool OUT_F32>
 __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
-  extern __shared__ __align__(16) uint16_t smem[];
-  uint16_t* s_k = smem;                 // [2][BN * D]
-  uint16_t* s_vt = smem + 2 * BN * D;   // [2][D * BN]
+  using L = FwdLayout<D>;
+  extern __shared__ __align__(16) char smem[];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -163,27 +87,59 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 
   // Q columns for the B operand: lane half lh holds dims 16kk + 8lh .. +7.
   bf16x8 qf[D / 16];
-  {
-    const uint16_t* qp = p.q + (q_row * p.hq + h) * D + lh * 8;
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-      qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 16);
-  }
+  load_frags<D>(qf, p.q, q_row, p.hq, h, lh);
 
   f32x16 oacc[D / 32];
 #pragma unroll
-  for (int cc = 0; cc < D / 32; ++cc)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[cc][r] = 0.f;
-  float m = -INFINITY;  // running max of scaled scores (log2 units)
-  float l = 0.f;        // this lane's share of the running row sum
+  for (int cc = 0; cc < D / 32; ++cc) zero(oacc[cc]);
+  float m = -INFINITY;  // reference max of scaled scores (log2 units)
+  float l = 0.f;        // this lane's share of the row sum
 
   if (run_b < run_e) {
-    Stage<D> st;
+    // Per-thread byte offsets that stay fixed for the whole item.
+    const int c = tid % L::CPR;
+    const int r0 = tid / L::CPR;
+    const int64_t row_elems = int64_t{p.hkv} * D;  // elements per KV row
+    const uint32_t g_voff = static_cast<uint32_t>((r0 * row_elems + c * 8) * 2);
+    const uint32_t g_step = static_cast<uint32_t>(L::RSTEP * row_elems * 2);
+    const uint32_t blk_bytes = static_cast<uint32_t>(BN * row_elems * 2);
+    const int k_w = r0 * L::KSTR + c * 16;
+    const int v_w = L::KBYTES + r0 * L::VSTR + c * 16;
+    // K operand read: row kt*32 + perm(li), 16 bytes at dims 16kk + 8lh.
+    const int k_r = key_perm(li) * L::KSTR + lh * 16;
+    // V^T operand read (transpose): 16-lane group g, lane s: row
+    // 8*(g>>1) + s/4 (+16ss, +4 for the second half), dims
+    // 16*(g&1) + 4*(s%4) (+32cc).
+    const int grp = lane >> 4, s16 = lane & 15;
+    const int v_r = L::KBYTES + (8 * (grp >> 1) + (s16 >> 2)) * L::VSTR +
+                    (16 * (grp & 1) + 4 * (s16 & 3)) * 2;
+
+    u32x4 kreg[L::NLD], vreg[L::NLD];
+    auto gload = [&](int64_t blk) {
+      const int64_t e0 = (blk * BN * p.hkv + hk) * D;
+      const rsrc_t rk = make_rsrc(p.k + e0, blk_bytes);
+      const rsrc_t rv = make_rsrc(p.v + e0, blk_bytes);
+#pragma unroll
+      for (int i = 0; i < L::NLD; ++i) {
+        kreg[i] = buffer_load16(rk, g_voff, i * g_step);
+        vreg[i] = buffer_load16(rv, g_voff, i * g_step);
+      }
+    };
+    auto lstore = [&](int stage) {
+      char* base = smem + stage * L::STAGE;
+#pragma unroll
+      for (int i = 0; i < L::NLD; ++i) {
+        *reinterpret_cast<u32x4*>(base + k_w + i * L::RSTEP * L::KSTR) =
+            kreg[i];
+        *reinterpret_cast<u32x4*>(base + v_w + i * L::RSTEP * L::VSTR) =
+            vreg[i];
+      }
+    };
+
     int r = run_b, off = 0;
     DevRun cur = p.runs[r];
-    st.load(p.k, p.v, cur.blk0, p.hkv, hk, tid);
-    st.store(s_k, s_vt, tid);
+    gload(cur.blk0);
+    lstore(0);
     __syncthreads();
     int stage = 0;
     while (true) {
@@ -197,23 +153,20 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
       DevRun nxt = cur;
       if (has_next) {
         nxt = p.runs[nr];
-        st.load(p.k, p.v, int64_t{nxt.blk0} + noff, p.hkv, hk, tid);
+        gload(int64_t{nxt.blk0} + noff);
       }
 
-      const uint16_t* sk = s_k + stage * BN * D;
-      const uint16_t* svt = s_vt + stage * D * BN;
+      const char* sb = smem + stage * L::STAGE;
 
       // S^T = K Q^T for two 32-key tiles.
       f32x16 s[2];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s[kt][i] = 0.f;
-        const int row = kt * 32 + key_perm(li);
+        zero(s[kt]);
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) {
           const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              sk + row * D + k_chunk<D>(row, 2 * kk + lh) * 8);
+              sb + k_r + kt * 32 * L::KSTR + kk * 32);
           s[kt] = mfma32(a, qf[kk], s[kt]);
         }
       }
@@ -225,60 +178,53 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = kt * 32 + (i >> 3) * 16 + lh * 8 + (i & 7);
-            if (key > lim) s[kt][i] = -INFINITY;
-          }
+          for (int i = 0; i < 16; ++i)
+            if (kt * 32 + acc_row(i, lh) > lim) s[kt][i] = -INFINITY;
       }
 
-      // Online softmax (log2 domain).
+      // Online softmax (log2 domain), rescaling only on a large max jump.
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kt][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m, mx * p.scale_log2);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = fast_exp2(m - m_use);
-      float rs = 0.f;
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.scale_log2;
+      const bool need = mx > m;
+      if (__builtin_amdgcn_ballot_w64(need)) {
+        const float m_new = need ? mx : m;
+        const float alpha = exp2_fast(m - m_new);  // 1 if unchanged, 0 from -inf
+        l *= alpha;
+#pragma unroll
+        for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
+        m = m_new;
+      }
+      const float m_use = (m == -INFINITY) ? 0.f : m;
+      bf16x8 pb[4];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float e = fast_exp2(fmaf(s[kt][i], p.scale_log2, -m_use));
-          s[kt][i] = e;
-          rs += e;
+          const float e = exp2_fast(fmaf(s[kt][i], p.scale_log2, -m_use));
+          l += e;
+          pb[kt * 2 + (i >> 3)][i & 7] = static_cast<__bf16>(e);
         }
-      l = l * alpha + rs;
-      m = m_new;
-#pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
 
-      // P^T as B operand: key step ss covers keys 16ss + 8lh + 0..7.
-      bf16x8 pb[4];
-#pragma unroll
-      for (int ss = 0; ss < 4; ++ss)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          pb[ss][e] = static_cast<__bf16>(s[ss >> 1][(ss & 1) * 8 + e]);
-
-      // O^T += V^T P^T.
+      // O^T += V^T P^T; key step ss covers keys 16ss + 8lh + 0..7.
 #pragma unroll
       for (int cc = 0; cc < D / 32; ++cc) {
-        const int dim = cc * 32 + li;
 #pragma unroll
         for (int ss = 0; ss < 4; ++ss) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              svt + dim * BN + vt_chunk(dim, 2 * ss + lh) * 8);
+          const char* a0 = sb + v_r + ss * 16 * L::VSTR + cc * 64;
+          const bf16x8 a =
+              join_bf16(lds_read_tr16(a0), lds_read_tr16(a0 + 4 * L::VSTR));
           oacc[cc] = mfma32(a, pb[ss], oacc[cc]);
         }
       }
 
       if (!has_next) break;
-      st.store(s_k + (stage ^ 1) * BN * D, s_vt + (stage ^ 1) * D * BN, tid);
+      lstore(stage ^ 1);
       __syncthreads();
       stage ^= 1;
       r = nr;
@@ -287,7 +233,7 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
     }
   }
 
-  // Epilogue: O = acc / l, LSE = ln(sum) = (m + log2 l) * ln 2.
+  // Epilogue: O = acc / l, LSE = (m + log2 l) * ln 2.
   const float lt = l + __shfl_xor(l, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
   if (lh == 0) {
@@ -303,21 +249,15 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int dim = cc * 32 + g * 8 + lh * 4;
-      const float x0 = oacc[cc][4 * g + 0] * inv;
-      const float x1 = oacc[cc][4 * g + 1] * inv;
-      const float x2 = oacc[cc][4 * g + 2] * inv;
-      const float x3 = oacc[cc][4 * g + 3] * inv;
+      f32x4 x;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) x[t] = oacc[cc][4 * g + t] * inv;
       if constexpr (OUT_F32) {
-        float4 val = make_float4(x0, x1, x2, x3);
-        *reinterpret_cast<float4*>(static_cast<float*>(p.o) + obase + dim) =
-            val;
+        *reinterpret_cast<f32x4*>(static_cast<float*>(p.o) + obase + dim) = x;
       } else {
-        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
         bf16x4 val;
-        val[0] = static_cast<__bf16>(x0);
-        val[1] = static_cast<__bf16>(x1);
-        val[2] = static_cast<__bf16>(x2);
-        val[3] = static_cast<__bf16>(x3);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) val[t] = static_cast<__bf16>(x[t]);
         *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(p.o) + obase + dim) =
             val;
       }
@@ -326,7 +266,7 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 
 template <int D, bool F32>
 hipError_t launch(const FwdParams& p, int grid, hipStream_t stream) {
-  const size_t smem = 2 * (2 * BN * D) * sizeof(uint16_t);
+  const size_t smem = FwdLayout<D>::SMEM;
   auto kern = tile_fwd_kernel<D, F32>;
   static bool attr_done = false;  // benign race: idempotent attribute set
   if (!attr_done) {
