@@ -37,6 +37,38 @@ __device__ __forceinline__ float exp2_fast(float x) {
   return __builtin_amdgcn_exp2f(x);
 }
 
+// Read-only kernel data (work lists) through the constant address space: the
+// compiler may then always use scalar loads for uniform addresses, whatever
+// else the kernel does.
+template <typename T>
+__device__ __forceinline__ T load_const(const T* p, int64_t i) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef const __attribute__((address_space(4))) T* cptr;
+  T v;
+  __builtin_memcpy(&v, (cptr)(p) + i, sizeof(T));
+  return v;
+#else
+  return p[i];
+#endif
+}
+
+// Make the compiler wait here for the loads that produced `v` (an empty asm
+// that reads the registers).  Used before a loop so the wait analysis at the
+// loop header sees these registers as complete; unlike an s_waitcnt
+// intrinsic it has no memory effect, so uniform loads stay scalar.
+template <typename T>
+__device__ __forceinline__ void wait_for(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+
+// max(x, x of the lane 32 apart): v_permlane32_swap exchanges the two
+// half-waves of a register pair in the VALU, without an LDS round trip.
+__device__ __forceinline__ float max_with_other_half(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto sw = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+
 __device__ __forceinline__ void zero(f32x16& a) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) a[i] = 0.f;

@@ -74,13 +74,13 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  const int2 item = p.order[blockIdx.x];
+  const int2 item = load_const(p.order, blockIdx.x);
   if (item.x < 0) return;
   const int qblk = item.x;
   const int h = item.y;
   const int hk = h / p.group;
-  const int run_b = p.qblk_ptr[qblk];
-  const int run_e = p.qblk_ptr[qblk + 1];
+  const int run_b = load_const(p.qblk_ptr, qblk);
+  const int run_e = load_const(p.qblk_ptr, qblk + 1);
 
   const int64_t q_row = int64_t{qblk} * BM + wave * 32 + li;
   const int q_in_blk = wave * 32 + li;
@@ -137,9 +137,13 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
     };
 
     int r = run_b, off = 0;
-    DevRun cur = p.runs[r];
+    DevRun cur = load_const(p.runs, r);
     gload(cur.blk0);
     lstore(0);
+    // Complete the Q fragment loads here, so the loop never waits on them
+    // behind the next block's prefetch.
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) wait_for(qf[kk]);
     __syncthreads();
     int stage = 0;
     while (true) {
@@ -152,7 +156,7 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
       const bool has_next = nr < run_e;
       DevRun nxt = cur;
       if (has_next) {
-        nxt = p.runs[nr];
+        nxt = load_const(p.runs, nr);
         gload(int64_t{nxt.blk0} + noff);
       }
 
@@ -188,7 +192,7 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kt][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.scale_log2;
+      mx = max_with_other_half(mx) * p.scale_log2;
       const bool need = mx > m;
       if (__builtin_amdgcn_ballot_w64(need)) {
         const float m_new = need ? mx : m;
@@ -202,14 +206,20 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
       }
       const float m_use = (m == -INFINITY) ? 0.f : m;
       bf16x8 pb[4];
+      float rs[4];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int ss = 0; ss < 4; ++ss) {
+        float e8[8];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float e = exp2_fast(fmaf(s[kt][i], p.scale_log2, -m_use));
-          l += e;
-          pb[kt * 2 + (i >> 3)][i & 7] = static_cast<__bf16>(e);
+        for (int e = 0; e < 8; ++e) {
+          e8[e] = exp2_fast(
+              fmaf(s[ss >> 1][(ss & 1) * 8 + e], p.scale_log2, -m_use));
+          pb[ss][e] = static_cast<__bf16>(e8[e]);
         }
+        rs[ss] = ((e8[0] + e8[1]) + (e8[2] + e8[3])) +
+                 ((e8[4] + e8[5]) + (e8[6] + e8[7]));
+      }
+      l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
 
       // O^T += V^T P^T; key step ss covers keys 16ss + 8lh + 0..7.
 #pragma unroll
