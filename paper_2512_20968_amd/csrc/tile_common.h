@@ -205,6 +205,25 @@ __device__ __forceinline__ u32x4 buffer_load16(rsrc_t r, uint32_t voff,
                                                static_cast<int>(soff), 0);
 }
 
+// Direct global -> LDS load of 16 bytes per lane (buffer_load_dwordx4 ... lds):
+// lane i of the wave writes LDS bytes [lds + 16 i, lds + 16 i + 16) with the
+// 16 bytes at buffer offset voff + soff.  `lds` must be wave-uniform.  The
+// load is counted by vmcnt; the data is in LDS once vmcnt has drained.
+__device__ __forceinline__ void buffer_load16_lds(rsrc_t r, void* lds,
+                                                  uint32_t voff,
+                                                  uint32_t soff) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(lds), 16,
+                                           static_cast<int>(voff),
+                                           static_cast<int>(soff), 0, 0);
+}
+
+// s_waitcnt vmcnt(0): this wave's vector-memory loads (including those
+// written straight into LDS) have completed.
+__device__ __forceinline__ void wait_vmem() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+
 // ---------------------------------------------------------------------------
 // LDS transpose read (gfx950 ds_read_b64_tr_b16).  Within each group of 16
 // lanes, lane s supplies the address of 4 consecutive bf16 values x[s][0..3];

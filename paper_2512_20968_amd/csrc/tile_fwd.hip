@@ -49,16 +49,52 @@ constexpr int NT = kThreads;
 
 template <int D>
 struct FwdLayout {
-  static constexpr int KSTR = 2 * D + 16;   // K tile row stride, bytes
-  static constexpr int VSTR = 2 * D + 64;   // V tile row stride, bytes
-  static constexpr int KBYTES = BN * KSTR;
-  static constexpr int VBYTES = BN * VSTR;
-  static constexpr int STAGE = KBYTES + VBYTES;
-  static constexpr int SMEM = 2 * STAGE;
-  static constexpr int CPR = D / 8;         // 16-byte chunks per row
-  static constexpr int RSTEP = NT / CPR;    // rows per load pass
-  static constexpr int NLD = BN / RSTEP;    // loads per thread per tensor
+  static constexpr int ROWB = 2 * D;         // bytes per K/V row
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;       // rows per 1 KB wave load
+  static constexpr int RPW = BN / 4;         // rows each wave loads
+  static constexpr int NLI = RPW / RPI;      // wave loads per tile
+  static constexpr int TILE = BN * ROWB;     // bytes per K or V tile
+  static constexpr int SMEM = 4 * TILE;      // K0, K1, V0, V1
+  // XOR swizzles of the 16-byte chunk index, chosen so that the MFMA operand
+  // reads below hit distinct LDS banks.
+  __device__ static int kswz(int row) {
+    return D == 128 ? (row & 15) : ((row >> 1) & 7);
+  }
+  __device__ static int vswz(int row) {
+    return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
+  }
 };
+
+// Position in the flattened list of KV blocks of one Q block's runs.
+struct Cursor {
+  DevRun run;
+  int r, off;
+  bool valid;
+  __device__ int64_t blk() const { return int64_t{run.blk0} + off; }
+};
+
+__device__ __forceinline__ Cursor first_block(const FwdParams& p, int r) {
+  Cursor c;
+  c.run = load_const(p.runs, r);
+  c.r = r;
+  c.off = 0;
+  c.valid = true;
+  return c;
+}
+
+__device__ __forceinline__ Cursor next_block(const FwdParams& p, Cursor c,
+                                             int run_e) {
+  if (!c.valid) return c;
+  if (++c.off == c.run.nblk) {
+    c.off = 0;
+    if (++c.r < run_e)
+      c.run = load_const(p.runs, c.r);
+    else
+      c.valid = false;
+  }
+  return c;
+}
 
 // Row order of a 32-key tile as fed to the MFMA: swap bits 2 and 3.
 __device__ __forceinline__ int key_perm(int r) { return mfma_row_perm(r); }
@@ -69,7 +105,9 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
   extern __shared__ __align__(16) char smem[];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  // Wave index as a scalar (the compiler cannot infer that tid >> 6 is
+  // uniform across the wave).
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int li = lane & 31;
   const int lh = lane >> 5;
@@ -96,103 +134,178 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
   float l = 0.f;        // this lane's share of the row sum
 
   if (run_b < run_e) {
-    // Per-thread byte offsets that stay fixed for the whole item.
-    const int c = tid % L::CPR;
-    const int r0 = tid / L::CPR;
+    // Direct global -> LDS staging.  Wave `wave` fills rows
+    // wave*RPW .. +RPW of a tile with NLI loads of 1 KB; lane i of load j
+    // takes row wave*RPW + j*RPI + i/CPR and writes physical chunk i%CPR,
+    // i.e. the logical chunk (i%CPR) ^ swizzle(row).
     const int64_t row_elems = int64_t{p.hkv} * D;  // elements per KV row
-    const uint32_t g_voff = static_cast<uint32_t>((r0 * row_elems + c * 8) * 2);
-    const uint32_t g_step = static_cast<uint32_t>(L::RSTEP * row_elems * 2);
+    const uint32_t row_bytes_g = static_cast<uint32_t>(row_elems * 2);
     const uint32_t blk_bytes = static_cast<uint32_t>(BN * row_elems * 2);
-    const int k_w = r0 * L::KSTR + c * 16;
-    const int v_w = L::KBYTES + r0 * L::VSTR + c * 16;
-    // K operand read: row kt*32 + perm(li), 16 bytes at dims 16kk + 8lh.
-    const int k_r = key_perm(li) * L::KSTR + lh * 16;
-    // V^T operand read (transpose): 16-lane group g, lane s: row
-    // 8*(g>>1) + s/4 (+16ss, +4 for the second half), dims
-    // 16*(g&1) + 4*(s%4) (+32cc).
-    const int grp = lane >> 4, s16 = lane & 15;
-    const int v_r = L::KBYTES + (8 * (grp >> 1) + (s16 >> 2)) * L::VSTR +
-                    (16 * (grp & 1) + 4 * (s16 & 3)) * 2;
-
-    u32x4 kreg[L::NLD], vreg[L::NLD];
-    auto gload = [&](int64_t blk) {
-      const int64_t e0 = (blk * BN * p.hkv + hk) * D;
-      const rsrc_t rk = make_rsrc(p.k + e0, blk_bytes);
-      const rsrc_t rv = make_rsrc(p.v + e0, blk_bytes);
+    uint32_t kvo[L::NLI], vvo[L::NLI];
 #pragma unroll
-      for (int i = 0; i < L::NLD; ++i) {
-        kreg[i] = buffer_load16(rk, g_voff, i * g_step);
-        vreg[i] = buffer_load16(rv, g_voff, i * g_step);
+    for (int j = 0; j < L::NLI; ++j) {
+      const int row = wave * L::RPW + j * L::RPI + lane / L::CPR;
+      const int phys = lane % L::CPR;
+      kvo[j] = (lane / L::CPR) * row_bytes_g + ((phys ^ L::kswz(row)) * 16);
+      vvo[j] = (lane / L::CPR) * row_bytes_g + ((phys ^ L::vswz(row)) * 16);
+    }
+    auto rsrc_of = [&](const uint16_t* base, int64_t blk) {
+      return make_rsrc(base + (blk * BN * p.hkv + hk) * D, blk_bytes);
+    };
+    // LDS: K buffers 0, 1 then V buffers 0, 1.
+    auto load_k = [&](int64_t blk, int buf) {
+      const rsrc_t rk = rsrc_of(p.k, blk);
+#pragma unroll
+      for (int j = 0; j < L::NLI; ++j) {
+        const int row0 = wave * L::RPW + j * L::RPI;
+        buffer_load16_lds(rk, smem + buf * L::TILE + row0 * L::ROWB, kvo[j],
+                          row0 * row_bytes_g);
       }
     };
-    auto lstore = [&](int stage) {
-      char* base = smem + stage * L::STAGE;
+    auto load_v = [&](int64_t blk, int buf) {
+      const rsrc_t rv = rsrc_of(p.v, blk);
 #pragma unroll
-      for (int i = 0; i < L::NLD; ++i) {
-        *reinterpret_cast<u32x4*>(base + k_w + i * L::RSTEP * L::KSTR) =
-            kreg[i];
-        *reinterpret_cast<u32x4*>(base + v_w + i * L::RSTEP * L::VSTR) =
-            vreg[i];
+      for (int j = 0; j < L::NLI; ++j) {
+        const int row0 = wave * L::RPW + j * L::RPI;
+        buffer_load16_lds(rv, smem + (2 + buf) * L::TILE + row0 * L::ROWB,
+                          vvo[j], row0 * row_bytes_g);
       }
     };
-
-    int r = run_b, off = 0;
-    DevRun cur = load_const(p.runs, r);
-    gload(cur.blk0);
-    lstore(0);
-    // Complete the Q fragment loads here, so the loop never waits on them
-    // behind the next block's prefetch.
+    // K operand read: row kt*32 + perm(li), dims 16kk + 8lh (logical chunk
+    // 2kk + lh); the swizzle of such a row does not depend on kt.
+    int kra[D / 16];
+    {
+      const int prow = key_perm(li);
+      const int ks = L::kswz(prow);
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) wait_for(qf[kk]);
-    __syncthreads();
-    int stage = 0;
-    while (true) {
-      // Next block of the flattened run list.
-      int nr = r, noff = off + 1;
-      if (noff == cur.nblk) {
-        nr = r + 1;
-        noff = 0;
+      for (int kk = 0; kk < D / 16; ++kk)
+        kra[kk] = prow * L::ROWB + (((2 * kk + lh) ^ ks) * 16);
+    }
+    // V^T operand read (transpose): 16-lane group g, lane s reads row
+    // 8*(g>>1) + s/4 (+16ss, +4 for the second half) at dims
+    // 32cc + 16*(g&1) + 4*(s%4) .. +3; the swizzle of those rows depends on
+    // s only.
+    int vra[D / 32];
+    {
+      const int grp = lane >> 4, s16 = lane & 15;
+      const int vrow = 8 * (grp >> 1) + (s16 >> 2);
+      const int vs = L::vswz(vrow);
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) {
+        const int c16 = 4 * cc + 2 * (grp & 1) + ((s16 & 3) >> 1);
+        vra[cc] = 2 * L::TILE + vrow * L::ROWB + ((c16 ^ vs) * 16) +
+                  8 * (s16 & 1);
       }
-      const bool has_next = nr < run_e;
-      DevRun nxt = cur;
-      if (has_next) {
-        nxt = load_const(p.runs, nr);
-        gload(int64_t{nxt.blk0} + noff);
-      }
+    }
 
-      const char* sb = smem + stage * L::STAGE;
-
-      // S^T = K Q^T for two 32-key tiles.
-      f32x16 s[2];
+    // S^T = K Q^T of one 64-key block from K buffer `buf`.
+    auto scores = [&](f32x16 (&sc)[2], int buf) {
+      const char* kb = smem + buf * L::TILE;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        zero(s[kt]);
+        zero(sc[kt]);
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              sb + k_r + kt * 32 * L::KSTR + kk * 32);
-          s[kt] = mfma32(a, qf[kk], s[kt]);
-        }
+        for (int kk = 0; kk < D / 16; ++kk)
+          sc[kt] = mfma32(*reinterpret_cast<const bf16x8*>(
+                              kb + kra[kk] + kt * 32 * L::ROWB),
+                          qf[kk], sc[kt]);
       }
-
-      // Causal mask on PARTIAL runs: key j of the run is hidden from query i
-      // of the block iff j - i > delta.
-      if (cur.cls == 1) {
-        const int lim = cur.delta - off * BN + q_in_blk;
+    };
+    // Causal mask of a PARTIAL block: key j of the run is hidden from query
+    // i of the Q block iff j - i > delta.
+    auto apply_mask = [&](f32x16 (&sc)[2], const Cursor& cu) {
+      const int lim = cu.run.delta - cu.off * BN + q_in_blk;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            if (kt * 32 + acc_row(i, lh) > lim) s[kt][i] = -INFINITY;
-      }
-
-      // Online softmax (log2 domain), rescaling only on a large max jump.
+        for (int i = 0; i < 16; ++i)
+          if (kt * 32 + acc_row(i, lh) > lim) sc[kt][i] = -INFINITY;
+    };
+    // Scaled row max (both half-waves hold the same query row).
+    auto row_max = [&](const f32x16 (&sc)[2]) {
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kt][i]);
-      mx = max_with_other_half(mx) * p.scale_log2;
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[kt][i]);
+      return max_with_other_half(mx) * p.scale_log2;
+    };
+
+    // Pipeline: iteration n computes P of block n and O += V(n)^T P(n)^T,
+    // and meanwhile the scores of block n+1.  K runs one block ahead of V:
+    // during iteration n, K buffer (n+1)&1 holds K(n+1) and V buffer n&1
+    // holds V(n); K(n+2) and V(n+1) stream straight into the other buffers.
+    Cursor cur = first_block(p, run_b);   // block n
+    Cursor nx = next_block(p, cur, run_e);  // block n+1
+    Cursor nn = next_block(p, nx, run_e);   // block n+2
+    load_k(cur.blk(), 0);
+    load_v(cur.blk(), 0);
+    if (nx.valid) load_k(nx.blk(), 1);
+    // Complete the Q fragment loads and the first tiles here, so the loop
+    // never waits on them behind the next block's prefetch.
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) wait_for(qf[kk]);
+    wait_vmem();
+    __syncthreads();
+
+    f32x16 s_cur[2];
+    scores(s_cur, 0);
+    if (cur.run.cls == 1) apply_mask(s_cur, cur);
+    m = row_max(s_cur);  // first block: nothing to rescale yet
+    // Every wave has read K(0) before iteration 0 refills K buffer 0.
+    __syncthreads();
+    int ph = 0;  // n & 1
+    while (true) {
+      // K(n+2) -> K buffer n&1 (K(n) was consumed last iteration) and
+      // V(n+1) -> V buffer (n+1)&1 (V(n-1) likewise), straight into LDS.
+      if (nn.valid) load_k(nn.blk(), ph);
+      if (nx.valid) load_v(nx.blk(), ph ^ 1);
+
+      // --- one scheduling region: no branches until the row max ---------
+      // P(n) = exp2(s S(n) - m), row sums, bf16 B operand ...
+      const float m_use = (m == -INFINITY) ? 0.f : m;
+      bf16x8 pb[4];
+      float rs[4];
+#pragma unroll
+      for (int ss = 0; ss < 4; ++ss) {
+        float e8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          e8[e] = exp2_fast(
+              fmaf(s_cur[ss >> 1][(ss & 1) * 8 + e], p.scale_log2, -m_use));
+          pb[ss][e] = static_cast<__bf16>(e8[e]);
+        }
+        rs[ss] = ((e8[0] + e8[1]) + (e8[2] + e8[3])) +
+                 ((e8[4] + e8[5]) + (e8[6] + e8[7]));
+      }
+      l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
+      // ... the scores of block n+1 (independent of the exponentials; after
+      // the last block they read a stale buffer and are discarded) ...
+      f32x16 s_nxt[2];
+      scores(s_nxt, ph ^ 1);
+      // ... then O^T += V(n)^T P(n)^T (key step ss: keys 16ss + 8lh + 0..7)
+      const char* vb = smem + ph * L::TILE;
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) {
+#pragma unroll
+        for (int ss = 0; ss < 4; ++ss) {
+          const char* a0 = vb + vra[cc] + ss * 16 * L::ROWB;
+          const bf16x8 a =
+              join_bf16(lds_read_tr16(a0), lds_read_tr16(a0 + 4 * L::ROWB));
+          oacc[cc] = mfma32(a, pb[ss], oacc[cc]);
+        }
+      }
+      // ... with the unmasked row max of block n+1 alongside.
+      float mx = row_max(s_nxt);
+      // --------------------------------------------------------------------
+      if (!nx.valid) break;
+      if (nx.run.cls == 1) {
+        apply_mask(s_nxt, nx);
+        mx = row_max(s_nxt);
+      }
+
+      // Running max with block n+1; rescale O and l only if some row of the
+      // wave has a new max (exact max: a row's largest probability stays 1).
       const bool need = mx > m;
       if (__builtin_amdgcn_ballot_w64(need)) {
         const float m_new = need ? mx : m;
@@ -204,42 +317,15 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
           for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
         m = m_new;
       }
-      const float m_use = (m == -INFINITY) ? 0.f : m;
-      bf16x8 pb[4];
-      float rs[4];
-#pragma unroll
-      for (int ss = 0; ss < 4; ++ss) {
-        float e8[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          e8[e] = exp2_fast(
-              fmaf(s[ss >> 1][(ss & 1) * 8 + e], p.scale_log2, -m_use));
-          pb[ss][e] = static_cast<__bf16>(e8[e]);
-        }
-        rs[ss] = ((e8[0] + e8[1]) + (e8[2] + e8[3])) +
-                 ((e8[4] + e8[5]) + (e8[6] + e8[7]));
-      }
-      l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
 
-      // O^T += V^T P^T; key step ss covers keys 16ss + 8lh + 0..7.
-#pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) {
-#pragma unroll
-        for (int ss = 0; ss < 4; ++ss) {
-          const char* a0 = sb + v_r + ss * 16 * L::VSTR + cc * 64;
-          const bf16x8 a =
-              join_bf16(lds_read_tr16(a0), lds_read_tr16(a0 + 4 * L::VSTR));
-          oacc[cc] = mfma32(a, pb[ss], oacc[cc]);
-        }
-      }
-
-      if (!has_next) break;
-      lstore(stage ^ 1);
+      wait_vmem();
       __syncthreads();
-      stage ^= 1;
-      r = nr;
-      off = noff;
-      cur = nxt;
+      s_cur[0] = s_nxt[0];
+      s_cur[1] = s_nxt[1];
+      cur = nx;
+      nx = nn;
+      nn = next_block(p, nn, run_e);
+      ph ^= 1;
     }
   }
 
