@@ -114,7 +114,7 @@ def cpu_baseline(cfg, budget_s):
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": used,
             "kind": "oracle",
             "sample": (f"float64 oracle forward of {len(rows)} sampled query "
-                       f"rows x {done_heads} heads of the causal 64K tile "
+                       f"rows x {done_heads} heads of the {cfg.name} tile "
                        f"({flops / 1e9:.1f} GFLOP algorithmic, {dt:.1f} s)")}
 
 
@@ -249,7 +249,9 @@ def main():
     if "merge" in legs:
         mbytes = (mk * mrows * mh * (md * 2 + 4) + mrows * mh * (md * 2 + 4))
         gbs = mbytes / (leg_ms["merge"] * 1e-3) / 1e9
+        mdig = source_digest(["lse_merge.hip", "internal.h"])
         out_legs["merge"] = {"ms": round(leg_ms["merge"], 4),
+                             "traffic": load_traffic("lse_merge", mdig),
                              "GB/s": round(gbs, 1),
                              "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
                              "bytes": mbytes,
@@ -283,10 +285,12 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16 Q/K/V/dO)",
-        "config": {"workload": "causal-64k tile: 65536 tokens in 16 "
-                               "partitions of 4096; Q partitions 4..7 x KV "
-                               "partitions 0..7; 32 heads, head_dim 128; "
-                               "step = fwd + lse_merge(16x4096x32x128) + bwd",
+        "config": {"workload": f"{cfg.name} tile: {cfg.note}; "
+                               f"{hq} q heads / {hkv} kv heads, head_dim {d}"
+                               f"; step = " + " + ".join(
+                                   {"fwd": "tile_fwd", "merge":
+                                    "lse_merge(16x4096x32x128)",
+                                    "bwd": "tile_bwd"}[x] for x in legs),
                    "legs": legs},
         "roofline": roofline,
         "cpu_baseline": cpu,
