@@ -11,8 +11,8 @@ namespace mesh_attn {
 // XCDs round robin, so id i runs on XCD i % 8.
 constexpr int kNumXcd = 8;
 
-// Forward block shape: 4 waves x 32 query rows, 64 keys per LDS stage.
-constexpr int kFwdBM = 128;
+// Forward block shape: 8 waves x 32 query rows, 64 keys per LDS stage.
+constexpr int kFwdBM = 256;
 constexpr int kFwdBN = 64;
 
 // Backward block shapes.

@@ -52,6 +52,19 @@ __device__ __forceinline__ T load_const(const T* p, int64_t i) {
 #endif
 }
 
+// Workgroup barrier for LDS-only hand-offs: waits for this wave's own LDS
+// (and scalar) accesses, then s_barrier.  Unlike __syncthreads() it does not
+// drain outstanding global loads, so loads streaming into LDS may stay in
+// flight across it; the code that issued them waits (vmcnt) before the
+// barrier that publishes their buffer.  The empty asm statements keep the
+// compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Make the compiler wait here for the loads that produced `v` (an empty asm
 // that reads the registers).  Used before a loop so the wait analysis at the
 // loop header sees these registers as complete; unlike an s_waitcnt

@@ -1,12 +1,20 @@
 // Tile attention forward for gfx950 (MI355X).
 //
-// One workgroup computes one (Q block, query head) item: BM = 128 query rows,
-// four waves of 32 rows each.  It walks the Q block's runs of KV blocks
+// One workgroup computes one (Q block, query head) item: BM = 256 query rows,
+// eight waves of 32 rows each.  It walks the Q block's runs of KV blocks
 // (BN = 64 keys each) from the work list, so EMPTY blocks are never touched
 // and only PARTIAL runs evaluate the causal mask (a wave-uniform branch).  For
 // every KV block it forms scores, updates the online softmax of each row and
 // accumulates P V -- the per-pair computation of Algorithm 2 with the
 // online-softmax reducer applied inside the kernel (Section 2.2).
+//
+// Schedule: two-group ping-pong.  Waves 0-3 (group A) and 4-7 (group B)
+// share the four SIMDs pairwise (wave w and w+4 on SIMD w % 4).  Per KV block
+// each wave runs an MFMA phase X(n) -- the scores of block n+1 and
+// O += V(n)^T P(n)^T -- and a VALU phase Y(n) -- mask, running max, rescale
+// and the exponentials that make P(n+1).  Group B runs one phase behind
+// group A and every phase ends at a workgroup barrier, so on each SIMD one
+// wave's MFMAs always overlap the other wave's softmax.
 //
 // Layout choices (64-wide wavefronts, v_mfma_f32_32x32x16_bf16):
 //  * Scores are computed transposed, S^T = K Q^T (A = K rows from LDS,
@@ -16,21 +24,14 @@
 //  * K rows are fed to the MFMA in an order that swaps bits 2 and 3 of the
 //    row index, which leaves P^T in the accumulators already laid out as the
 //    k-contiguous B operand of O^T += V^T P^T.
-//  * K and V tiles are stored row-major in LDS with padded rows (272 B and
-//    320 B for d = 128), conflict-free for the reads below and affine in the
-//    loop indices, so every LDS read is one base register plus an immediate.
-//  * The V^T operand comes straight from the row-major V tile through the
-//    LDS transpose read (ds_read_b64_tr_b16), two per MFMA.
-//  * Global loads are raw buffer loads: scalar base per KV block, one
-//    per-lane offset register, scalar per-load offsets.  The next block's
-//    loads are issued before the current block's MFMAs; K/V tiles are double
-//    buffered in LDS with one barrier per block.
+//  * K and V tiles stream from HBM straight into LDS (buffer loads with the
+//    LDS-destination form, no staging registers), double buffered, rows
+//    XOR-swizzled so every MFMA operand read is bank-conflict free.
+//  * The V^T operand comes from the row-major V tile through the LDS
+//    transpose read (ds_read_b64_tr_b16), two per MFMA.
 //  * Softmax runs in the log2 domain with the scale folded into one FMA
-//    before v_exp_f32.  The running max is exact (the largest probability of
-//    a row is exactly 1, which keeps its bf16 rounding error-free), but the
-//    O rescale is skipped when no row of the wave has a new max -- a
-//    wave-uniform branch taken on a small fraction of blocks once the max has
-//    settled.
+//    before v_exp_f32.  The running max is exact, so a row's largest
+//    probability is exactly 1 and its bf16 rounding is error-free.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -43,16 +44,18 @@ namespace {
 
 using namespace dev;
 
-constexpr int BM = kFwdBM;  // 128
+constexpr int BM = kFwdBM;  // 256
 constexpr int BN = kFwdBN;  // 64
-constexpr int NT = kThreads;
+constexpr int NW = 8;       // waves per workgroup
+constexpr int NT = NW * 64;
+static_assert(BM == NW * 32, "one 32-row tile per wave");
 
 template <int D>
 struct FwdLayout {
   static constexpr int ROWB = 2 * D;         // bytes per K/V row
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;       // rows per 1 KB wave load
-  static constexpr int RPW = BN / 4;         // rows each wave loads
+  static constexpr int RPW = BN / 4;         // rows each loading wave loads
   static constexpr int NLI = RPW / RPI;      // wave loads per tile
   static constexpr int TILE = BN * ROWB;     // bytes per K or V tile
   static constexpr int SMEM = 4 * TILE;      // K0, K1, V0, V1
@@ -74,12 +77,13 @@ struct Cursor {
   __device__ int64_t blk() const { return int64_t{run.blk0} + off; }
 };
 
-__device__ __forceinline__ Cursor first_block(const FwdParams& p, int r) {
+__device__ __forceinline__ Cursor first_block(const FwdParams& p, int r,
+                                              int run_e) {
   Cursor c;
-  c.run = load_const(p.runs, r);
   c.r = r;
   c.off = 0;
-  c.valid = true;
+  c.valid = r < run_e;
+  if (c.valid) c.run = load_const(p.runs, r);
   return c;
 }
 
@@ -100,7 +104,7 @@ __device__ __forceinline__ Cursor next_block(const FwdParams& p, Cursor c,
 __device__ __forceinline__ int key_perm(int r) { return mfma_row_perm(r); }
 
 template <int D, bool OUT_F32>
-__global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
   using L = FwdLayout<D>;
   extern __shared__ __align__(16) char smem[];
 
@@ -108,6 +112,8 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
   // Wave index as a scalar (the compiler cannot infer that tid >> 6 is
   // uniform across the wave).
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;   // 0: group A, 1: group B
+  const int wg = wave & 3;     // wave within its group
   const int lane = tid & 63;
   const int li = lane & 31;
   const int lh = lane >> 5;
@@ -133,69 +139,72 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
   float m = -INFINITY;  // reference max of scaled scores (log2 units)
   float l = 0.f;        // this lane's share of the row sum
 
-  if (run_b < run_e) {
-    // Direct global -> LDS staging.  Wave `wave` fills rows
-    // wave*RPW .. +RPW of a tile with NLI loads of 1 KB; lane i of load j
-    // takes row wave*RPW + j*RPI + i/CPR and writes physical chunk i%CPR,
-    // i.e. the logical chunk (i%CPR) ^ swizzle(row).
+  // Number of KV blocks of this Q block.
+  int nblocks = 0;
+  for (int r = run_b; r < run_e; ++r) nblocks += load_const(p.runs, r).nblk;
+
+  if (nblocks > 0) {
+    // Direct global -> LDS staging, done by the four waves of group B.
+    // Wave wg of the group fills rows wg*RPW .. +RPW of a tile with NLI
+    // loads of 1 KB; lane i of load j takes row wg*RPW + j*RPI + i/CPR and
+    // writes physical chunk i%CPR, i.e. the logical chunk
+    // (i%CPR) ^ swizzle(row).
     const int64_t row_elems = int64_t{p.hkv} * D;  // elements per KV row
     const uint32_t row_bytes_g = static_cast<uint32_t>(row_elems * 2);
     const uint32_t blk_bytes = static_cast<uint32_t>(BN * row_elems * 2);
-    uint32_t kvo[L::NLI], vvo[L::NLI];
-#pragma unroll
-    for (int j = 0; j < L::NLI; ++j) {
-      const int row = wave * L::RPW + j * L::RPI + lane / L::CPR;
-      const int phys = lane % L::CPR;
-      kvo[j] = (lane / L::CPR) * row_bytes_g + ((phys ^ L::kswz(row)) * 16);
-      vvo[j] = (lane / L::CPR) * row_bytes_g + ((phys ^ L::vswz(row)) * 16);
-    }
+    // Every swizzled offset below has the form base ^ (stride * index): the
+    // swizzle XORs a lane-dependent value into the chunk bits, and the loop
+    // index only flips higher chunk bits that the row part leaves zero.  So
+    // one base register per stream plus a v_xor per access replaces a
+    // register per access.
+    // Loads: lane i of load j reads logical chunk (i%CPR) ^ swizzle(row) of
+    // row wg*RPW + j*RPI + i/CPR; for K that is kvo0 ^ (64 j), for V the
+    // swizzle does not depend on j.
+    const int lrow = lane / L::CPR;
+    const uint32_t kvo0 =
+        lrow * row_bytes_g + (((lane % L::CPR) ^ L::kswz(wg * L::RPW + lrow)) * 16);
+    const uint32_t vvo0 =
+        lrow * row_bytes_g + (((lane % L::CPR) ^ L::vswz(wg * L::RPW + lrow)) * 16);
     auto rsrc_of = [&](const uint16_t* base, int64_t blk) {
       return make_rsrc(base + (blk * BN * p.hkv + hk) * D, blk_bytes);
     };
-    // LDS: K buffers 0, 1 then V buffers 0, 1.
+    // LDS: K buffers 0, 1 then V buffers 0, 1; block j uses buffers j & 1.
     auto load_k = [&](int64_t blk, int buf) {
       const rsrc_t rk = rsrc_of(p.k, blk);
 #pragma unroll
       for (int j = 0; j < L::NLI; ++j) {
-        const int row0 = wave * L::RPW + j * L::RPI;
-        buffer_load16_lds(rk, smem + buf * L::TILE + row0 * L::ROWB, kvo[j],
-                          row0 * row_bytes_g);
+        const int row0 = wg * L::RPW + j * L::RPI;
+        buffer_load16_lds(rk, smem + buf * L::TILE + row0 * L::ROWB,
+                          kvo0 ^ (64u * j), row0 * row_bytes_g);
       }
     };
     auto load_v = [&](int64_t blk, int buf) {
       const rsrc_t rv = rsrc_of(p.v, blk);
 #pragma unroll
       for (int j = 0; j < L::NLI; ++j) {
-        const int row0 = wave * L::RPW + j * L::RPI;
+        const int row0 = wg * L::RPW + j * L::RPI;
         buffer_load16_lds(rv, smem + (2 + buf) * L::TILE + row0 * L::ROWB,
-                          vvo[j], row0 * row_bytes_g);
+                          vvo0, row0 * row_bytes_g);
       }
     };
     // K operand read: row kt*32 + perm(li), dims 16kk + 8lh (logical chunk
-    // 2kk + lh); the swizzle of such a row does not depend on kt.
-    int kra[D / 16];
+    // 2kk + lh); the swizzle of such a row does not depend on kt, and the
+    // byte offset is kra0 ^ (32 kk).
+    int kra0;
     {
       const int prow = key_perm(li);
-      const int ks = L::kswz(prow);
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-        kra[kk] = prow * L::ROWB + (((2 * kk + lh) ^ ks) * 16);
+      kra0 = prow * L::ROWB + ((lh ^ L::kswz(prow)) * 16);
     }
     // V^T operand read (transpose): 16-lane group g, lane s reads row
     // 8*(g>>1) + s/4 (+16ss, +4 for the second half) at dims
     // 32cc + 16*(g&1) + 4*(s%4) .. +3; the swizzle of those rows depends on
-    // s only.
-    int vra[D / 32];
+    // s only, and the byte offset is vra0 ^ (64 cc).
+    int vra0;
     {
-      const int grp = lane >> 4, s16 = lane & 15;
-      const int vrow = 8 * (grp >> 1) + (s16 >> 2);
-      const int vs = L::vswz(vrow);
-#pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) {
-        const int c16 = 4 * cc + 2 * (grp & 1) + ((s16 & 3) >> 1);
-        vra[cc] = 2 * L::TILE + vrow * L::ROWB + ((c16 ^ vs) * 16) +
-                  8 * (s16 & 1);
-      }
+      const int g16 = lane >> 4, s16 = lane & 15;
+      const int vrow = 8 * (g16 >> 1) + (s16 >> 2);
+      const int c16 = 2 * (g16 & 1) + ((s16 & 3) >> 1);
+      vra0 = vrow * L::ROWB + ((c16 ^ L::vswz(vrow)) * 16) + 8 * (s16 & 1);
     }
 
     // S^T = K Q^T of one 64-key block from K buffer `buf`.
@@ -207,64 +216,76 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk)
           sc[kt] = mfma32(*reinterpret_cast<const bf16x8*>(
-                              kb + kra[kk] + kt * 32 * L::ROWB),
+                              kb + (kra0 ^ (32 * kk)) + kt * 32 * L::ROWB),
                           qf[kk], sc[kt]);
       }
-    };
-    // Causal mask of a PARTIAL block: key j of the run is hidden from query
-    // i of the Q block iff j - i > delta.
-    auto apply_mask = [&](f32x16 (&sc)[2], const Cursor& cu) {
-      const int lim = cu.run.delta - cu.off * BN + q_in_blk;
+      // Keep three operand reads in flight ahead of the MFMAs instead of
+      // hoisting all of them (which would cost ~64 registers).
+      constexpr int NM = D / 8;  // MFMAs in this block
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if (kt * 32 + acc_row(i, lh) > lim) sc[kt][i] = -INFINITY;
+      for (int i = 0; i < NM - 3; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
     };
-    // Scaled row max (both half-waves hold the same query row).
-    auto row_max = [&](const f32x16 (&sc)[2]) {
+    // O^T += V^T P^T from V buffer `buf`; key step ss covers keys
+    // 16ss + 8lh + 0..7.
+    auto pv = [&](const bf16x8 (&pb)[4], int buf) {
+      const char* vb = smem + (2 + buf) * L::TILE;
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) {
+#pragma unroll
+        for (int ss = 0; ss < 4; ++ss) {
+          const char* a0 = vb + (vra0 ^ (64 * cc)) + ss * 16 * L::ROWB;
+          const bf16x8 a =
+              join_bf16(lds_read_tr16(a0), lds_read_tr16(a0 + 4 * L::ROWB));
+          oacc[cc] = mfma32(a, pb[ss], oacc[cc]);
+        }
+      }
+      // Two transpose reads per MFMA, three MFMAs' worth in flight.
+      constexpr int NM = D / 8;
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+      for (int i = 0; i < NM - 3; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+    };
+    // Softmax of one block's scores: causal mask (PARTIAL blocks: key j of
+    // the run is hidden from query i of the Q block iff j - i > delta),
+    // running max, rescale of O and l if some row of the wave has a new max,
+    // then P = exp2(s S - m) into the bf16 B operand and the row sums.
+    auto softmax = [&](f32x16 (&sc)[2], const Cursor& cu, bf16x8 (&pb)[4]) {
+      if (cu.run.cls == 1) {
+        const int lim = cu.run.delta - cu.off * BN + q_in_blk;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if (kt * 32 + acc_row(i, lh) > lim) sc[kt][i] = -INFINITY;
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[kt][i]);
-      return max_with_other_half(mx) * p.scale_log2;
-    };
-
-    // Pipeline: iteration n computes P of block n and O += V(n)^T P(n)^T,
-    // and meanwhile the scores of block n+1.  K runs one block ahead of V:
-    // during iteration n, K buffer (n+1)&1 holds K(n+1) and V buffer n&1
-    // holds V(n); K(n+2) and V(n+1) stream straight into the other buffers.
-    Cursor cur = first_block(p, run_b);   // block n
-    Cursor nx = next_block(p, cur, run_e);  // block n+1
-    Cursor nn = next_block(p, nx, run_e);   // block n+2
-    load_k(cur.blk(), 0);
-    load_v(cur.blk(), 0);
-    if (nx.valid) load_k(nx.blk(), 1);
-    // Complete the Q fragment loads and the first tiles here, so the loop
-    // never waits on them behind the next block's prefetch.
+      mx = max_with_other_half(mx) * p.scale_log2;
+      // Rescale unconditionally: alpha is exactly 1 when the max did not
+      // change, and the multiplies fit in this phase's VALU slack (the other
+      // group's MFMA phase is longer), while a branch here would push the
+      // kernel past its register budget.
+      const float m_new = fmaxf(m, mx);
+      const float alpha = exp2_fast(m - m_new);  // 1 if unchanged, 0 from -inf
+      l *= alpha;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) wait_for(qf[kk]);
-    wait_vmem();
-    __syncthreads();
-
-    f32x16 s_cur[2];
-    scores(s_cur, 0);
-    if (cur.run.cls == 1) apply_mask(s_cur, cur);
-    m = row_max(s_cur);  // first block: nothing to rescale yet
-    // Every wave has read K(0) before iteration 0 refills K buffer 0.
-    __syncthreads();
-    int ph = 0;  // n & 1
-    while (true) {
-      // K(n+2) -> K buffer n&1 (K(n) was consumed last iteration) and
-      // V(n+1) -> V buffer (n+1)&1 (V(n-1) likewise), straight into LDS.
-      if (nn.valid) load_k(nn.blk(), ph);
-      if (nx.valid) load_v(nx.blk(), ph ^ 1);
-
-      // --- one scheduling region: no branches until the row max ---------
-      // P(n) = exp2(s S(n) - m), row sums, bf16 B operand ...
+      for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
+      m = m_new;
       const float m_use = (m == -INFINITY) ? 0.f : m;
-      bf16x8 pb[4];
       float rs[4];
 #pragma unroll
       for (int ss = 0; ss < 4; ++ss) {
@@ -272,60 +293,83 @@ __global__ __launch_bounds__(NT, 2) void tile_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           e8[e] = exp2_fast(
-              fmaf(s_cur[ss >> 1][(ss & 1) * 8 + e], p.scale_log2, -m_use));
+              fmaf(sc[ss >> 1][(ss & 1) * 8 + e], p.scale_log2, -m_use));
           pb[ss][e] = static_cast<__bf16>(e8[e]);
         }
         rs[ss] = ((e8[0] + e8[1]) + (e8[2] + e8[3])) +
                  ((e8[4] + e8[5]) + (e8[6] + e8[7]));
       }
       l += (rs[0] + rs[1]) + (rs[2] + rs[3]);
-      // ... the scores of block n+1 (independent of the exponentials; after
-      // the last block they read a stale buffer and are discarded) ...
-      f32x16 s_nxt[2];
-      scores(s_nxt, ph ^ 1);
-      // ... then O^T += V(n)^T P(n)^T (key step ss: keys 16ss + 8lh + 0..7)
-      const char* vb = smem + ph * L::TILE;
+    };
+
+    // Prologue (all waves): K(0), V(0) and K(1) into LDS (group B loads),
+    // then the scores and probabilities of block 0.
+    Cursor c0 = first_block(p, run_b, run_e);
+    Cursor c1 = next_block(p, c0, run_e);
+    if (grp == 1) {
+      load_k(c0.blk(), 0);
+      load_v(c0.blk(), 0);
+      if (c1.valid) load_k(c1.blk(), 1);
+    }
 #pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) {
-#pragma unroll
-        for (int ss = 0; ss < 4; ++ss) {
-          const char* a0 = vb + vra[cc] + ss * 16 * L::ROWB;
-          const bf16x8 a =
-              join_bf16(lds_read_tr16(a0), lds_read_tr16(a0 + 4 * L::ROWB));
-          oacc[cc] = mfma32(a, pb[ss], oacc[cc]);
+    for (int kk = 0; kk < D / 16; ++kk) wait_for(qf[kk]);
+    wait_vmem();
+    __syncthreads();
+    bf16x8 pb[4];
+    {
+      f32x16 s0[2];
+      scores(s0, 0);
+      softmax(s0, c0, pb);
+    }
+    // Every wave has read K(0) before group B refills K buffer 0.
+    __syncthreads();
+
+    // Phase loops.  There are 2N slots (N = nblocks), each ending at a
+    // workgroup barrier (an LDS-only barrier: group B's loads stay in flight
+    // across the barrier of the slot that issues them).  Group A runs X(0) Y(0) X(1) ... X(N-1) and idles in
+    // the last slot; group B idles in the first slot and then runs the same
+    // sequence, one slot behind.  Group B issues the loads of K(n+2) and
+    // V(n+1) in slot 2n and drains them at the end of slot 2n+1, so they are
+    // in LDS by slot 2n+2, when A's X(n+1) first reads them; the buffers they
+    // overwrite were last read in slots 2n-2 and 2n-1.
+    f32x16 snx[2];
+    Cursor cs = c1;  // block whose scores X(n) computes (block n+1)
+    if (grp == 0) {
+      for (int n = 0; n < nblocks; ++n) {
+        if (cs.valid) scores(snx, (n + 1) & 1);
+        pv(pb, n & 1);
+        lds_barrier();
+        if (cs.valid) {
+          softmax(snx, cs, pb);
+          cs = next_block(p, cs, run_e);
+        }
+        lds_barrier();
+      }
+    } else {
+      Cursor ck = next_block(p, c1, run_e);  // K block to load next
+      Cursor cv = c1;                        // V block to load next
+      auto issue_loads = [&](int n) {  // slot 2n: K(n+2), V(n+1)
+        if (ck.valid) load_k(ck.blk(), n & 1);
+        if (cv.valid) load_v(cv.blk(), (n + 1) & 1);
+        ck = next_block(p, ck, run_e);
+        cv = next_block(p, cv, run_e);
+      };
+      issue_loads(0);
+      lds_barrier();
+      for (int n = 0; n < nblocks; ++n) {
+        if (cs.valid) scores(snx, (n + 1) & 1);
+        pv(pb, n & 1);
+        wait_vmem();
+        lds_barrier();
+        if (cs.valid) {
+          softmax(snx, cs, pb);
+          cs = next_block(p, cs, run_e);
+        }
+        if (n + 1 < nblocks) {  // the last slot belongs to X(N-1)
+          issue_loads(n + 1);
+          lds_barrier();
         }
       }
-      // ... with the unmasked row max of block n+1 alongside.
-      float mx = row_max(s_nxt);
-      // --------------------------------------------------------------------
-      if (!nx.valid) break;
-      if (nx.run.cls == 1) {
-        apply_mask(s_nxt, nx);
-        mx = row_max(s_nxt);
-      }
-
-      // Running max with block n+1; rescale O and l only if some row of the
-      // wave has a new max (exact max: a row's largest probability stays 1).
-      const bool need = mx > m;
-      if (__builtin_amdgcn_ballot_w64(need)) {
-        const float m_new = need ? mx : m;
-        const float alpha = exp2_fast(m - m_new);  // 1 if unchanged, 0 from -inf
-        l *= alpha;
-#pragma unroll
-        for (int cc = 0; cc < D / 32; ++cc)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
-        m = m_new;
-      }
-
-      wait_vmem();
-      __syncthreads();
-      s_cur[0] = s_nxt[0];
-      s_cur[1] = s_nxt[1];
-      cur = nx;
-      nx = nn;
-      nn = next_block(p, nn, run_e);
-      ph ^= 1;
     }
   }
 
