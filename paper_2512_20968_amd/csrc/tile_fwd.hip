@@ -273,19 +273,22 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[kt][i]);
       mx = max_with_other_half(mx) * p.scale_log2;
-      // Rescale unconditionally: alpha is exactly 1 when the max did not
-      // change, and the multiplies fit in this phase's VALU slack (the other
-      // group's MFMA phase is longer), while a branch here would push the
-      // kernel past its register budget.
+      // Rescale O and l only when some row of the wave has a new maximum
+      // (a wave-uniform branch).  Past the first few blocks of a row that is
+      // rare, and the 4 * D / 2 multiplies would otherwise be the largest
+      // VALU item of this phase after the exponentials.  A row whose maximum
+      // is still -inf takes alpha = exp2(-inf) = 0 on 0-valued sums.
       const float m_new = fmaxf(m, mx);
-      const float alpha = exp2_fast(m - m_new);  // 1 if unchanged, 0 from -inf
-      l *= alpha;
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      if (__builtin_amdgcn_ballot_w64(m_new != m)) {
+        const float alpha = exp2_fast(m - m_use);
+        l *= alpha;
 #pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc)
+        for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
-      m = m_new;
-      const float m_use = (m == -INFINITY) ? 0.f : m;
+          for (int i = 0; i < 16; ++i) oacc[cc][i] *= alpha;
+        m = m_new;
+      }
       float rs[4];
 #pragma unroll
       for (int ss = 0; ss < 4; ++ss) {
