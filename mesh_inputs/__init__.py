@@ -6,7 +6,7 @@ arithmetic.  All draws use a CPU ``torch.Generator`` so that both sides see
 bit-identical bfloat16 tensors.
 
 The workloads stand in for one GPU's share of the paper's runs (BF16, head dim
-128, contiguous partitions of a long sequence; Section 4.1).  The paper uses no
+128, contiguous or striped partitions of a long sequence; Sections 3.7, 4.1).  The paper uses no
 dataset: its inputs are random activations of the attention operator, so i.i.d.
 N(0, 1) tensors cast to bfloat16 have the paper's shapes and value range.
 """
@@ -31,6 +31,7 @@ class TileConfig:
     seed: int
     outliers: bool = False    # one Q row and one K row per partition scaled x8
     grad_seed: Optional[int] = None   # seed of dO for a backward workload
+    layout: int = 0           # 0: contiguous partitions, 1: striped positions
     note: str = field(default="", compare=False)
 
     @property
@@ -54,7 +55,8 @@ class TileConfig:
                     num_kv_heads=self.num_kv_heads,
                     head_dim=self.head_dim,
                     causal=int(self.causal),
-                    softmax_scale=self.softmax_scale)
+                    softmax_scale=self.softmax_scale,
+                    layout=self.layout)
 
 
 CONFIGS = {
@@ -73,6 +75,17 @@ CONFIGS = {
     5: TileConfig("bwd-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
                   32, 32, 128, True, seed=1, grad_seed=4,
                   note="backward of the causal-64k tile; dO from seed 4"),
+    # Striped layout (token r of partition p at position r*n + p): every
+    # partition pair is near-triangular, so every tile of a mesh carries about
+    # the same causal work.
+    6: TileConfig("striped-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
+                  32, 32, 128, True, seed=5, grad_seed=6, layout=1,
+                  note="65536 tokens striped over 16 partitions of 4096, "
+                       "tile {4..7}x{0..7}; dO from seed 6"),
+    7: TileConfig("striped-mesh1m-causal", 256, 4096, list(range(24, 40)),
+                  list(range(16, 32)), 32, 32, 128, True, seed=7, layout=1,
+                  note="1M tokens striped over 256 partitions, 16x16 tile "
+                       "Q24..39 x KV16..31"),
 }
 
 

@@ -13,7 +13,8 @@ against the paper by eye, not for speed:
 * ``attention``  -- the attention definition (Section 2.1), the partial
   ``(O, lse)`` of a Q partition over a KV partition set (Section 2.2), the
   online-softmax reducer used to merge partials (Section 2.2, Algorithm 2), the
-  causal rule on global token positions (Section 3.7), GQA head sharing
+  causal rule on global token positions under the contiguous and the striped
+  sequence layouts (Section 3.7), GQA head sharing
   (Section 4.8), and the attention gradients the backward pass of Algorithm 3
   needs.
 * ``worklist``   -- classification of the tile's (Q block, KV block) pairs into
@@ -30,7 +31,10 @@ examples the paper prints (``tests/golden``).
 """
 
 from .attention import (  # noqa: F401
+    CONTIGUOUS,
+    STRIPED,
     token_positions,
+    problem_positions,
     attention_rows,
     lse_merge,
     attention_rows_bwd,

@@ -16,16 +16,42 @@ import numpy as np
 NEG_INF = -np.inf
 
 
-def token_positions(part_ids, part_len):
+CONTIGUOUS, STRIPED = 0, 1
+
+
+def token_positions(part_ids, part_len, layout=CONTIGUOUS, num_partitions=None):
     """Global token position of every row of a stacked partition buffer.
 
-    The sequence is split evenly and contiguously (Section 2.2: Q, K and V are
-    split evenly along the sequence dimension), so token ``r`` of partition
-    ``p`` sits at position ``p * P + r``.
+    ``layout = CONTIGUOUS``: the sequence is split evenly and contiguously
+    (Section 2.2: Q, K and V are split evenly along the sequence dimension),
+    so token ``r`` of partition ``p`` sits at position ``p * P + r``.
+
+    ``layout = STRIPED``: for causal attention Section 3.7 interleaves token
+    positions across the partitions (the striped layout of Striped Attention)
+    so that every tile holds a similar share of visible pairs.  The paper
+    gives no formula; the reading used here deals the positions round robin:
+    token ``r`` of partition ``p`` sits at position ``r * n + p``, with ``n``
+    = ``num_partitions``.
     """
     part_ids = np.asarray(part_ids, dtype=np.int64)
-    return (part_ids[:, None] * int(part_len)
-            + np.arange(int(part_len), dtype=np.int64)[None, :]).reshape(-1)
+    r = np.arange(int(part_len), dtype=np.int64)
+    if layout == CONTIGUOUS:
+        pos = part_ids[:, None] * int(part_len) + r[None, :]
+    elif layout == STRIPED:
+        n = int(num_partitions)
+        assert n >= 1 and np.all((part_ids >= 0) & (part_ids < n))
+        pos = r[None, :] * n + part_ids[:, None]
+    else:
+        raise ValueError(f"unknown layout {layout}")
+    return pos.reshape(-1)
+
+
+def problem_positions(prob, part_ids):
+    """``token_positions`` of a partition list under a problem description
+    (``partition_len``, ``num_partitions`` and optional ``layout``)."""
+    return token_positions(part_ids, prob["partition_len"],
+                           int(prob.get("layout", CONTIGUOUS)),
+                           prob.get("num_partitions"))
 
 
 def q_head_to_kv_head(h, num_q_heads, num_kv_heads):
@@ -151,7 +177,8 @@ def tile_forward(prob, q_idx, kv_idx, q, k, v, rows=None, heads=None,
     over the tile's KV footprint (the loop of Algorithm 1 / Algorithm 2).
 
     ``prob`` holds ``partition_len, num_q_heads, num_kv_heads, causal,
-    softmax_scale``.  ``q [nq*P, Hq, d]``, ``k, v [nkv*P, Hkv, d]`` (any float
+    softmax_scale`` and, for the striped layout, ``layout`` and
+    ``num_partitions`` (see ``token_positions``).  ``q [nq*P, Hq, d]``, ``k, v [nkv*P, Hkv, d]`` (any float
     dtype; widened exactly to float64).  ``rows`` selects tile rows of the Q
     buffer (default all), ``heads`` selects query heads (default all).
 
@@ -163,8 +190,8 @@ def tile_forward(prob, q_idx, kv_idx, q, k, v, rows=None, heads=None,
     hq, hkv = int(prob["num_q_heads"]), int(prob["num_kv_heads"])
     causal = bool(prob["causal"])
     scale = float(prob["softmax_scale"])
-    qpos = token_positions(q_idx, P)
-    kpos = token_positions(kv_idx, P)
+    qpos = problem_positions(prob, q_idx)
+    kpos = problem_positions(prob, kv_idx)
     rows = np.arange(qpos.shape[0]) if rows is None else np.asarray(rows)
     heads = list(range(hq)) if heads is None else list(heads)
     d = q.shape[2]
@@ -206,8 +233,8 @@ def tile_backward(prob, q_idx, kv_idx, q, k, v, do, kv_heads=None,
     causal = bool(prob["causal"])
     scale = float(prob["softmax_scale"])
     g = hq // hkv
-    qpos = token_positions(q_idx, P)
-    kpos = token_positions(kv_idx, P)
+    qpos = problem_positions(prob, q_idx)
+    kpos = problem_positions(prob, kv_idx)
     nrq, nrk = qpos.shape[0], kpos.shape[0]
     kv_heads = list(range(hkv)) if kv_heads is None else list(kv_heads)
     q_rows = np.arange(nrq) if q_rows is None else np.asarray(q_rows)

@@ -28,22 +28,25 @@ roles of the two sides (runs of Q blocks per KV block).
 
 import numpy as np
 
-from .attention import token_positions
+from .attention import CONTIGUOUS, token_positions
 
 EMPTY, PARTIAL, FULL = 0, 1, 2
 
 
-def classify_blocks(q_idx, kv_idx, part_len, bm, bn, causal):
+def classify_blocks(q_idx, kv_idx, part_len, bm, bn, causal,
+                    layout=CONTIGUOUS, num_partitions=None):
     """Class of every (Q block, KV block) pair from the extreme positions of
     the two blocks: EMPTY if the first key comes after the last query, FULL if
     the last key comes no later than the first query, PARTIAL otherwise.
+    Positions grow with the row inside a partition under both layouts, so a
+    block's first and last rows hold its extreme positions.
     Returns ``uint8 [nq*P/bm, nkv*P/bn]``."""
     P = int(part_len)
     assert P % bm == 0 and P % bn == 0
-    q_first = token_positions(q_idx, P)[::bm]
-    q_last = q_first + bm - 1
-    k_first = token_positions(kv_idx, P)[::bn]
-    k_last = k_first + bn - 1
+    qpos = token_positions(q_idx, P, layout, num_partitions)
+    kpos = token_positions(kv_idx, P, layout, num_partitions)
+    q_first, q_last = qpos[::bm], qpos[bm - 1::bm]
+    k_first, k_last = kpos[::bn], kpos[bn - 1::bn]
     if not causal:
         return np.full((q_first.size, k_first.size), FULL, dtype=np.uint8)
     cls = np.full((q_first.size, k_first.size), PARTIAL, dtype=np.uint8)
@@ -52,13 +55,14 @@ def classify_blocks(q_idx, kv_idx, part_len, bm, bn, causal):
     return cls
 
 
-def classify_blocks_bruteforce(q_idx, kv_idx, part_len, bm, bn, causal):
+def classify_blocks_bruteforce(q_idx, kv_idx, part_len, bm, bn, causal,
+                               layout=CONTIGUOUS, num_partitions=None):
     """Same classes from every single (query, key) pair of every block: FULL if
     all pairs are visible, EMPTY if none is, PARTIAL otherwise.  Cost grows with
     the number of token pairs; meant for small tiles."""
     P = int(part_len)
-    qpos = token_positions(q_idx, P)
-    kpos = token_positions(kv_idx, P)
+    qpos = token_positions(q_idx, P, layout, num_partitions)
+    kpos = token_positions(kv_idx, P, layout, num_partitions)
     nqb, nkb = qpos.size // bm, kpos.size // bn
     cls = np.empty((nqb, nkb), dtype=np.uint8)
     for qb in range(nqb):
