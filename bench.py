@@ -49,10 +49,15 @@ def visible_pairs(cfg):
         for kp in cfg.kv_idx:
             if not cfg.causal:
                 total += P * P
-                continue
-            k0 = kp * P
-            # keys k0..k0+P-1 visible to query at position x: clamp(x-k0+1)
-            total += int(np.clip(qpos - k0 + 1, 0, P).sum())
+            elif cfg.layout == 1:
+                # striped: key row r' visible to query row r iff
+                # r' * n + kp <= r * n + qp, i.e. r' <= r (kp <= qp) or
+                # r' < r (kp > qp)
+                total += P * (P + 1) // 2 - (P if kp > qp else 0)
+            else:
+                k0 = kp * P
+                # keys k0..k0+P-1 visible to query at position x: clamp(x-k0+1)
+                total += int(np.clip(qpos - k0 + 1, 0, P).sum())
     return total
 
 
@@ -124,10 +129,13 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--legs", default="fwd,merge,bwd")
-    ap.add_argument("--workload", type=int, default=2, choices=(2, 3, 4),
+    ap.add_argument("--workload", type=int, default=2,
+                    choices=(2, 3, 4, 6, 7),
                     help="forward tile: 2 causal 64K (default), 3 1M-token "
                          "non-causal GQA 16x16 tile, 4 1M-token causal 16x16 "
-                         "tile with outliers (backward always runs on 2)")
+                         "tile with outliers, 6 striped causal 64K, 7 "
+                         "striped 1M-token causal 16x16 tile (the backward "
+                         "leg runs on 2 and 6 only)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -149,7 +157,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = CONFIGS[args.workload]
-    if "bwd" in legs and args.workload != 2:
+    if "bwd" in legs and args.workload not in (2, 6):
         legs.remove("bwd")
     prob = cfg.problem()
     P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
@@ -164,7 +172,9 @@ def main():
     ws_f = torch.empty(ma.mesh_attn_fwd_workspace_size(prob, cfg.nq, cfg.nkv),
                        dtype=torch.uint8, device=dev)
     if "bwd" in legs:
-        do = make_grad(CONFIGS[5]).to(dev)
+        # dO of the backward workload of this tile (config 5 is the
+        # backward of config 2; config 6 carries its own gradient seed).
+        do = make_grad(CONFIGS[5] if args.workload == 2 else cfg).to(dev)
         dq = torch.empty((rq, hq, d), dtype=torch.float32, device=dev)
         dk = torch.empty((rkv, hkv, d), dtype=torch.float32, device=dev)
         dv = torch.empty_like(dk)

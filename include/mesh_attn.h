@@ -60,6 +60,14 @@ typedef enum { MA_BF16 = 0, MA_FP32 = 1 } ma_dtype_t;
 /* Block classes of a (Q block, KV block) pair under the causal rule. */
 enum { MA_CLS_EMPTY = 0, MA_CLS_PARTIAL = 1, MA_CLS_FULL = 2 };
 
+/* Sequence layout: which global position token r of partition p holds (it
+ * matters only for causal problems, Section 3.7).
+ *   MA_LAYOUT_CONTIGUOUS: position p * P + r (the even split of Section 2.2).
+ *   MA_LAYOUT_STRIPED:    position r * n + p (positions dealt round robin over
+ *                         the n partitions, the striped layout Section 3.7
+ *                         adopts to balance causal work across tiles). */
+enum { MA_LAYOUT_CONTIGUOUS = 0, MA_LAYOUT_STRIPED = 1 };
+
 typedef struct {
   int32_t num_partitions; /* n: partitions of the whole sequence, >= 1        */
   int32_t partition_len;  /* P: tokens per partition, multiple of the blocks  */
@@ -68,6 +76,8 @@ typedef struct {
   int32_t head_dim;       /* d: 64 or 128                                    */
   int32_t causal;         /* 0 or 1                                          */
   float softmax_scale;    /* s > 0, finite; usually 1/sqrt(d)                */
+  int32_t layout;         /* MA_LAYOUT_*; a key is visible to a query iff its
+                             position is not larger (causal problems)        */
 } ma_problem_t;
 
 /* ---------------------------------------------------------------------------

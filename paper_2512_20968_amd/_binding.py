@@ -36,7 +36,8 @@ class Problem(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32),
                 ("causal", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float),
+                ("layout", ctypes.c_int32)]
 
     @classmethod
     def make(cls, prob):
@@ -45,7 +46,7 @@ class Problem(ctypes.Structure):
         return cls(int(prob["num_partitions"]), int(prob["partition_len"]),
                    int(prob["num_q_heads"]), int(prob["num_kv_heads"]),
                    int(prob["head_dim"]), int(prob["causal"]),
-                   float(prob["softmax_scale"]))
+                   float(prob["softmax_scale"]), int(prob.get("layout", 0)))
 
 
 _lock = threading.Lock()

@@ -87,6 +87,9 @@ ma_status_t check_problem(const ma_problem_t* p) {
                 "num_kv_heads %d", p->num_q_heads, p->num_kv_heads);
   if (p->causal != 0 && p->causal != 1)
     return fail(MA_ERR_INVALID_ARG, "causal must be 0 or 1, got %d", p->causal);
+  if (p->layout != MA_LAYOUT_CONTIGUOUS && p->layout != MA_LAYOUT_STRIPED)
+    return fail(MA_ERR_INVALID_ARG, "layout must be %d or %d, got %d",
+                MA_LAYOUT_CONTIGUOUS, MA_LAYOUT_STRIPED, p->layout);
   if (!(p->softmax_scale > 0.f) || !std::isfinite(p->softmax_scale))
     return fail(MA_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   if (p->head_dim < 1)
@@ -111,6 +114,26 @@ ma_status_t check_tile(const ma_problem_t* p, const int32_t* q_idx, int32_t nq,
   st = check_list("q_idx", q_idx, nq, p->num_partitions);
   if (st != MA_OK) return st;
   return check_list("kv_idx", kv_idx, nkv, p->num_partitions);
+}
+
+// Global position of token `row` of partition `part` (Section 3.7 layouts).
+// Within a partition positions grow with the row under both layouts, so a
+// block's first and last rows hold its extreme positions.
+inline int64_t token_pos(const ma_problem_t* p, int32_t part, int64_t row) {
+  return p->layout == MA_LAYOUT_STRIPED
+             ? row * p->num_partitions + part
+             : int64_t{part} * p->partition_len + row;
+}
+
+// Mask offset of a (query block, key run) pair in rows: key row k0 + j is
+// hidden from query row q0 + i iff j - i > offset.  Contiguous: the position
+// difference q0 - k0 across partitions.  Striped: position (row * n + part),
+// so key after query iff (j - i) * n > (q0 - k0) * n + (qp - kp), i.e. iff
+// j - i > (q0 - k0) + floor((qp - kp) / n), and |qp - kp| < n.
+inline int64_t mask_offset(const ma_problem_t* p, int32_t qp, int64_t q0,
+                           int32_t kp, int64_t k0) {
+  if (p->layout == MA_LAYOUT_STRIPED) return (q0 - k0) + (qp >= kp ? 0 : -1);
+  return token_pos(p, qp, q0) - token_pos(p, kp, k0);
 }
 
 // Class of one block pair from its extreme token positions.
@@ -143,15 +166,17 @@ void build_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
     for (int32_t ab = 0; ab < nab; ++ab) {
       const int32_t row = a * nab + ab;
       (*ptr)[row] = static_cast<int32_t>(runs->size());
-      const int64_t a_first = a_idx[a] * P + int64_t{ab} * bm_a;
-      const int64_t a_last = a_first + bm_a - 1;
+      const int64_t a_first = token_pos(p, a_idx[a], int64_t{ab} * bm_a);
+      const int64_t a_last =
+          token_pos(p, a_idx[a], int64_t{ab} * bm_a + bm_a - 1);
       for (int32_t b = 0; b < nb; ++b) {
         int32_t kb = 0, cur = -1, start = 0;
         for (; kb <= nbb; ++kb) {
           int c = -2;
           if (kb < nbb) {
-            const int64_t b_first = b_idx[b] * P + int64_t{kb} * bm_b;
-            const int64_t b_last = b_first + bm_b - 1;
+            const int64_t b_first = token_pos(p, b_idx[b], int64_t{kb} * bm_b);
+            const int64_t b_last =
+                token_pos(p, b_idx[b], int64_t{kb} * bm_b + bm_b - 1);
             c = a_is_q ? block_class(a_first, a_last, b_first, b_last, causal)
                        : block_class(b_first, b_last, a_first, a_last, causal);
           }
@@ -226,6 +251,7 @@ std::string plan_key(int pass, const ma_problem_t* p, const int32_t* q_idx,
   put(&p->num_q_heads, sizeof(int32_t));
   put(&p->num_kv_heads, sizeof(int32_t));
   put(&p->causal, sizeof(int32_t));
+  put(&p->layout, sizeof(int32_t));
   put(&nq, sizeof nq);
   put(q_idx, sizeof(int32_t) * nq);
   put(&nkv, sizeof nkv);
@@ -234,8 +260,8 @@ std::string plan_key(int pass, const ma_problem_t* p, const int32_t* q_idx,
 }
 
 // Kernel-side runs of one orientation.  Side A blocks (bm_a rows) own the
-// workgroups; side B blocks (bm_b rows) are iterated.  delta = first position
-// of the query block/run minus first position of the key block/run.
+// workgroups; side B blocks (bm_b rows) are iterated.  delta = mask offset of
+// the query block/run against the key block/run (mask_offset).
 void device_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
                  int32_t bm_a, const int32_t* b_idx, int32_t nb, int32_t bm_b,
                  bool a_is_q, std::vector<int32_t>* ptr,
@@ -249,10 +275,12 @@ void device_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
   work->assign(ptr->size() - 1, 0);
   for (size_t i = 0; i < runs.size(); ++i) {
     const Run& r = runs[i];
-    const int64_t a_first =
-        a_idx[r.row / nab] * P + int64_t{r.row % nab} * bm_a;
-    const int64_t b_first = b_idx[r.list] * P + int64_t{r.begin} * bm_b;
-    const int64_t delta = a_is_q ? a_first - b_first : b_first - a_first;
+    const int32_t a_part = a_idx[r.row / nab];
+    const int64_t a_row0 = int64_t{r.row % nab} * bm_a;
+    const int32_t b_part = b_idx[r.list];
+    const int64_t b_row0 = int64_t{r.begin} * bm_b;
+    const int64_t delta = a_is_q ? mask_offset(p, a_part, a_row0, b_part, b_row0)
+                                 : mask_offset(p, b_part, b_row0, a_part, a_row0);
     (*out)[i] = DevRun{r.list * nbb + r.begin, r.end - r.begin, r.cls,
                        static_cast<int32_t>(delta)};
     (*work)[r.row] += r.end - r.begin;
@@ -434,12 +462,16 @@ ma_status_t mesh_attn_classify(const ma_problem_t* prob, const int32_t* q_idx,
   const int64_t nqb = nq * P / bm, nkb = nkv * P / bn;
   const int64_t qpb = P / bm, kpb = P / bn;
   for (int64_t qb = 0; qb < nqb; ++qb) {
-    const int64_t q_first = q_idx[qb / qpb] * P + (qb % qpb) * bm;
+    const int32_t qp = q_idx[qb / qpb];
+    const int64_t q_row = (qb % qpb) * bm;
+    const int64_t q_first = token_pos(prob, qp, q_row);
+    const int64_t q_last = token_pos(prob, qp, q_row + bm - 1);
     for (int64_t kb = 0; kb < nkb; ++kb) {
-      const int64_t k_first = kv_idx[kb / kpb] * P + (kb % kpb) * bn;
-      cls[qb * nkb + kb] = static_cast<uint8_t>(
-          block_class(q_first, q_first + bm - 1, k_first, k_first + bn - 1,
-                      prob->causal != 0));
+      const int32_t kp = kv_idx[kb / kpb];
+      const int64_t k_row = (kb % kpb) * bn;
+      cls[qb * nkb + kb] = static_cast<uint8_t>(block_class(
+          q_first, q_last, token_pos(prob, kp, k_row),
+          token_pos(prob, kp, k_row + bn - 1), prob->causal != 0));
     }
   }
   return ok();

@@ -42,7 +42,9 @@ def test_block_shape(pass_):
 
 def _check_bitexact(prob, q_idx, kv_idx, bm, bn):
     P = prob["partition_len"]
-    want_cls = oracle.classify_blocks(q_idx, kv_idx, P, bm, bn, prob["causal"])
+    want_cls = oracle.classify_blocks(q_idx, kv_idx, P, bm, bn, prob["causal"],
+                                      prob.get("layout", 0),
+                                      prob["num_partitions"])
     got_cls = ma.mesh_attn_classify(prob, q_idx, kv_idx, bm, bn)
     assert got_cls.dtype == np.uint8
     np.testing.assert_array_equal(got_cls, want_cls)
@@ -57,7 +59,7 @@ def _check_bitexact(prob, q_idx, kv_idx, bm, bn):
     np.testing.assert_array_equal(runs, want_runs)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6, 7])
 @pytest.mark.parametrize("pass_", [0, 1])
 def test_worklist_bitexact_on_configs(cid, pass_):
     cfg = CONFIGS[cid]
@@ -79,7 +81,8 @@ def test_worklist_bitexact_random_tiles():
                                              replace=False)]
         prob = dict(num_partitions=n, partition_len=P, num_q_heads=2,
                     num_kv_heads=1, head_dim=64,
-                    causal=int(rng.integers(0, 2)), softmax_scale=0.125)
+                    causal=int(rng.integers(0, 2)), softmax_scale=0.125,
+                    layout=int(rng.integers(0, 2)))
         _check_bitexact(prob, q_idx, kv_idx, bm, bn)
 
 
@@ -109,6 +112,8 @@ def _prob(**kw):
 @pytest.mark.parametrize("kw,q_idx,kv_idx,status", [
     (dict(num_q_heads=6, num_kv_heads=4), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
     (dict(causal=2), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
+    (dict(layout=2), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
+    (dict(layout=-1), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
     (dict(softmax_scale=0.0), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
     (dict(softmax_scale=float("nan")), [0], [0], ma._binding.MA_ERR_INVALID_ARG),
     ({}, [0, 4], [0], ma._binding.MA_ERR_INVALID_ARG),
