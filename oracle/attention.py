@@ -178,20 +178,29 @@ def tile_forward(prob, q_idx, kv_idx, q, k, v, rows=None, heads=None,
 
     ``prob`` holds ``partition_len, num_q_heads, num_kv_heads, causal,
     softmax_scale`` and, for the striped layout, ``layout`` and
-    ``num_partitions`` (see ``token_positions``).  ``q [nq*P, Hq, d]``, ``k, v [nkv*P, Hkv, d]`` (any float
-    dtype; widened exactly to float64).  ``rows`` selects tile rows of the Q
-    buffer (default all), ``heads`` selects query heads (default all).
+    ``num_partitions`` (see ``token_positions``).  ``q [nq*P, Hq, d]``,
+    ``k, v [nkv*P, Hkv, d]`` (any float dtype; widened exactly to float64).
+    ``rows`` selects tile rows of the Q buffer (default all), ``heads``
+    selects query heads (default all).
 
     The result equals attention over the concatenation of the tile's KV
     partitions, so it is computed in one pass per row here.  Returns
     ``o [len(rows), len(heads), d]`` and ``lse [len(heads), len(rows)]``.
     """
-    P = int(prob["partition_len"])
+    return forward_at_positions(prob, problem_positions(prob, q_idx),
+                                problem_positions(prob, kv_idx), q, k, v,
+                                rows, heads, row_chunk)
+
+
+def forward_at_positions(prob, qpos, kpos, q, k, v, rows=None, heads=None,
+                         row_chunk=256):
+    """``tile_forward`` for buffers whose rows sit at the given global
+    positions (``qpos [rows_q]``, ``kpos [rows_kv]``), e.g. the chunk buffers
+    of Section 3.4."""
     hq, hkv = int(prob["num_q_heads"]), int(prob["num_kv_heads"])
     causal = bool(prob["causal"])
     scale = float(prob["softmax_scale"])
-    qpos = problem_positions(prob, q_idx)
-    kpos = problem_positions(prob, kv_idx)
+    qpos, kpos = np.asarray(qpos), np.asarray(kpos)
     rows = np.arange(qpos.shape[0]) if rows is None else np.asarray(rows)
     heads = list(range(hq)) if heads is None else list(heads)
     d = q.shape[2]

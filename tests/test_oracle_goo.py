@@ -1,0 +1,137 @@
+"""Pins of the GOO oracle (Section 3.4): the paper's worked example (chunk
+token ranges and the planner's steps, tests/golden/goo_worked_example.json),
+schedule invariants on random instances, and the chunk compute tasks, whose
+running accumulation over the KV chunks must equal the unchunked tile."""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import goo
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "goo_worked_example.json")
+
+
+def _golden():
+    return json.load(open(GOLDEN))
+
+
+def test_worked_example_chunk_tokens():
+    g = _golden()
+    P = g["tokens_per_gpu"]
+    pos = oracle.token_positions(g["q_group"], P)
+    rows = goo.chunk_buffer_rows(P, len(g["q_group"]), g["k_q"], 0)
+    assert [int(x) for x in pos[rows]] == g["ag_q0_tokens"]
+    own = oracle.token_positions([4], P)
+    for i, want in enumerate(g["gpu4_q_chunks"]):
+        assert [int(own[r]) for r in goo.chunk_rows(P, g["k_q"], i)] == want
+
+
+def test_worked_example_schedule():
+    g = _golden()
+    c = g["costs"]
+    kq, kkv = g["k_q"], g["k_kv"]
+    t_c = [[c["c"]] * kkv for _ in range(kq)]
+    steps = goo.goo_plan(kq, kkv, c["ag_q"], c["ag_kv"], c["rs_q"], t_c,
+                         gamma=c["gamma"])
+    # 2 k_Q + k_KV collective steps plus the two compute-only steps
+    assert len(steps) == 2 * kq + kkv + len(g["compute_only_steps"])
+    for s, (kind, idx) in g["comm_of_step"].items():
+        assert steps[int(s) - 1][0] == (kind, idx), s
+    for s, tasks in g["tasks_of_step"].items():
+        assert sorted(steps[int(s) - 1][1]) == sorted(map(tuple, tasks)), s
+    only = [n + 1 for n, (comm, _) in enumerate(steps) if comm is None]
+    assert only == g["compute_only_steps"]
+    for n in only:
+        assert len(steps[n - 1][1]) == 1
+
+
+def _check_invariants(kq, kkv, tq, tkv, trs, t_c, gamma, steps):
+    seen_comm = {}
+    seen_task = {}
+    for n, (comm, tasks) in enumerate(steps):
+        if comm is None:
+            assert len(tasks) == 1
+        else:
+            assert comm not in seen_comm
+            seen_comm[comm] = n
+        for t in tasks:
+            assert t not in seen_task
+            seen_task[t] = n
+    assert set(seen_comm) == ({(goo.AG_Q, i) for i in range(kq)}
+                              | {(goo.AG_KV, j) for j in range(kkv)}
+                              | {(goo.RS_Q, i) for i in range(kq)})
+    assert set(seen_task) == {(i, j) for i in range(kq) for j in range(kkv)}
+    t_comm = {goo.AG_Q: tq, goo.AG_KV: tkv, goo.RS_Q: trs}
+    for (i, j), n in seen_task.items():
+        # ready when the step starts: both gathers in strictly earlier steps
+        assert seen_comm[(goo.AG_Q, i)] < n and seen_comm[(goo.AG_KV, j)] < n
+    for i in range(kq):
+        assert all(seen_task[(i, j)] < seen_comm[(goo.RS_Q, i)]
+                   for j in range(kkv))
+    for comm, tasks in steps:
+        if comm is None or not tasks:
+            continue
+        # just enough: without its last task the step was below its target
+        target = gamma * t_comm[comm[0]]
+        assert sum(t_c[i][j] for i, j in tasks[:-1]) < target
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_schedule_invariants_random(seed):
+    rng = np.random.default_rng(seed)
+    kq = int(rng.integers(1, 5))
+    kkv = int(rng.integers(1, max(2, 16 // kq) + 1))
+    kkv = min(kkv, 16 // kq)
+    tq, tkv, trs = (float(x) for x in rng.uniform(0.1, 2.0, 3))
+    t_c = rng.uniform(0.05, 1.5, (kq, kkv)).tolist()
+    gamma = float(rng.choice([1.0, 1.05, 1.2]))
+    steps = goo.goo_plan(kq, kkv, tq, tkv, trs, t_c, gamma)
+    _check_invariants(kq, kkv, tq, tkv, trs, t_c, gamma, steps)
+    # a serial schedule (every collective, then every task) is never faster
+    serial = kq * (tq + trs) + kkv * tkv + float(np.sum(t_c))
+    assert goo.plan_makespan(steps, tq, tkv, trs, t_c) <= serial + 1e-12
+
+
+def test_first_step_cannot_overlap_and_profit_rule():
+    """Nothing is ready before the first gather, so step 1 runs alone; when
+    one gather is cheaper per unlocked compute it goes first."""
+    steps = goo.goo_plan(2, 2, 1.0, 0.25, 0.5, [[1.0, 1.0], [1.0, 1.0]], 1.0)
+    assert steps[0][1] == []
+    # after AG-KV-0 (tie at zero profit, AG-KV first), AG-Q-0 unlocks 1.0
+    # for 1.0 (profit 1) and AG-KV-1 unlocks nothing: AG-Q-0 next.
+    assert steps[0][0] == (goo.AG_KV, 0) and steps[1][0] == (goo.AG_Q, 0)
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+@pytest.mark.parametrize("kq,kkv", [(2, 3), (4, 1), (1, 4)])
+def test_chunk_tasks_accumulate_to_the_tile(layout, kq, kkv):
+    """Running accumulation of C-i-0 .. C-i-(k_KV-1) equals the unchunked
+    tile on the rows of Q chunk i, for every i."""
+    n, P, d, hq, hkv = 4, 24, 8, 2, 1
+    prob = dict(num_partitions=n, partition_len=P, num_q_heads=hq,
+                num_kv_heads=hkv, head_dim=d, causal=1,
+                softmax_scale=1.0 / math.sqrt(d), layout=layout)
+    q_idx, kv_idx = [3, 1], [0, 2, 1]
+    rng = np.random.default_rng(5)
+    q = rng.standard_normal((len(q_idx) * P, hq, d))
+    k = rng.standard_normal((len(kv_idx) * P, hkv, d))
+    v = rng.standard_normal((len(kv_idx) * P, hkv, d))
+    o_tile, lse_tile = oracle.tile_forward(prob, q_idx, kv_idx, q, k, v)
+    for i in range(kq):
+        qr = goo.chunk_buffer_rows(P, len(q_idx), kq, i)
+        o_run = np.zeros((len(qr), hq, d))
+        lse_run = np.full((hq, len(qr)), -np.inf)
+        for j in range(kkv):
+            kr = goo.chunk_buffer_rows(P, len(kv_idx), kkv, j)
+            o_c, lse_c = goo.chunk_forward(prob, q_idx, kv_idx, kq, i, kkv, j,
+                                           q[qr], k[kr], v[kr])
+            o_run, lse_run = goo.accumulate_partial(o_run, lse_run, o_c, lse_c)
+        np.testing.assert_allclose(o_run, o_tile[qr], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse_run, lse_tile[:, qr], rtol=0,
+                                   atol=1e-12)
