@@ -27,7 +27,9 @@ Readings where the paper leaves a choice (the same in the library):
   the order AG-KV, AG-Q, RS-Q (the choices of the worked example);
 * among ready compute tasks the order is (Q chunk, KV chunk) ascending;
 * a step's fill stops at the first task that brings the total to the target
-  or above (the worked example's steps 3, 4 and 6).
+  or above (the worked example's steps 3, 4 and 6);
+* sums of task times run in ascending chunk order (profits) or in fill order
+  (step totals), so that the decisions are reproducible bit for bit.
 """
 
 import numpy as np
@@ -77,10 +79,12 @@ def goo_plan(k_q, k_kv, t_ag_q, t_ag_kv, t_rs_q, t_c, gamma=1.05):
         return sorted((i, j) for i in ag_q for j in ag_kv if (i, j) not in done)
 
     def unlock(kind, idx):
+        # summed in ascending chunk order, so that every implementation of the
+        # planner adds the same floating-point numbers in the same order
         if kind == AG_Q:
-            return sum(float(t_c[idx][j]) for j in ag_kv)
+            return sum(float(t_c[idx][j]) for j in range(k_kv) if j in ag_kv)
         if kind == AG_KV:
-            return sum(float(t_c[i][idx]) for i in ag_q)
+            return sum(float(t_c[i][idx]) for i in range(k_q) if i in ag_q)
         return 0.0
 
     while len(ag_q) < k_q or len(ag_kv) < k_kv or len(rs_q) < k_q:
