@@ -128,7 +128,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--legs", default="fwd,merge,bwd")
+    ap.add_argument("--legs", default="fwd,merge,bwd",
+                    help="comma list of fwd, merge, bwd, chunks (chunks: the "
+                         "forward of the same tile as k_Q x k_KV GOO chunk "
+                         "tasks, see --chunks)")
+    ap.add_argument("--chunks", default="4x4",
+                    help="k_Q x k_KV of the chunks leg")
     ap.add_argument("--workload", type=int, default=2,
                     choices=(2, 3, 4, 6, 7),
                     help="forward tile: 2 causal 64K (default), 3 1M-token "
@@ -181,6 +186,23 @@ def main():
         ws_b = torch.empty(ma.mesh_attn_bwd_workspace_size(prob, cfg.nq,
                                                            cfg.nkv),
                            dtype=torch.uint8, device=dev)
+    if "chunks" in legs:
+        # The buffers the chunk all-gathers would produce (chunk i of every
+        # Q partition, chunk j of every KV partition), built before timing.
+        kq, kkv = (int(x) for x in args.chunks.lower().split("x"))
+        cq, ckv = P // kq, P // kkv
+        def gather(t, n_parts, c, i):
+            return torch.cat([t[a * P + i * c:a * P + (i + 1) * c]
+                              for a in range(n_parts)]).contiguous()
+        cqd = [gather(qd, cfg.nq, cq, i) for i in range(kq)]
+        ckd = [gather(kd, cfg.nkv, ckv, j) for j in range(kkv)]
+        cvd = [gather(vd, cfg.nkv, ckv, j) for j in range(kkv)]
+        co = [torch.empty((cfg.nq * cq, hq, d), dtype=torch.float32,
+                          device=dev) for _ in range(kq)]
+        cl = [torch.empty((hq, cfg.nq * cq), dtype=torch.float32, device=dev)
+              for _ in range(kq)]
+        ws_c = torch.empty(ma.mesh_attn_chunk_fwd_workspace_size(
+            prob, cfg.nq, cfg.nkv), dtype=torch.uint8, device=dev)
     if "merge" in legs:
         mk, mrows, mh, md = 16, 4096, 32, 128
         mo_parts, ml_parts = make_merge_parts(mk, mrows, mh, md, seed=7)
@@ -196,6 +218,15 @@ def main():
             ma.mesh_attn_tile_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o,
                                   lse, ws=ws_f)
             if ev: ev["fwd"][1].record(stream)
+        if "chunks" in legs:
+            if ev: ev["chunks"][0].record(stream)
+            for i in range(kq):
+                for j in range(kkv):
+                    ma.mesh_attn_chunk_fwd(prob, cfg.q_idx, cfg.kv_idx,
+                                           (i, kq, j, kkv), cqd[i], ckd[j],
+                                           cvd[j], co[i], cl[i],
+                                           accumulate=int(j > 0), ws=ws_c)
+            if ev: ev["chunks"][1].record(stream)
         if "merge" in legs:
             if ev: ev["merge"][0].record(stream)
             ma.mesh_attn_lse_merge(mo_parts, ml_parts, mo, ml)
@@ -256,6 +287,14 @@ def main():
                            "tflops": round(tf, 2),
                            "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
                            "flop": fwd_flop}
+    if "chunks" in legs:
+        tc = fwd_flop / (leg_ms["chunks"] * 1e-3) / 1e12
+        out_legs["chunks"] = {"ms": round(leg_ms["chunks"], 4),
+                              "tflops": round(tc, 2),
+                              "frac_bf16_peak": round(tc / PEAK_BF16_TFLOPS,
+                                                      4),
+                              "chunks": f"{kq}x{kkv}",
+                              "launches": kq * kkv, "flop": fwd_flop}
     if "merge" in legs:
         mbytes = (mk * mrows * mh * (md * 2 + 4) + mrows * mh * (md * 2 + 4))
         gbs = mbytes / (leg_ms["merge"] * 1e-3) / 1e9
@@ -300,7 +339,9 @@ def main():
                                f"; step = " + " + ".join(
                                    {"fwd": "tile_fwd", "merge":
                                     "lse_merge(16x4096x32x128)",
-                                    "bwd": "tile_bwd"}[x] for x in legs),
+                                    "bwd": "tile_bwd",
+                                    "chunks": f"{args.chunks} chunk_fwd"}[x]
+                                   for x in legs),
                    "legs": legs},
         "roofline": roofline,
         "cpu_baseline": cpu,

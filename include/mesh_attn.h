@@ -155,6 +155,86 @@ ma_status_t mesh_attn_tile_fwd(const ma_problem_t* prob, const int32_t* q_idx,
                                void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Greedy Overlapping Optimization (GOO, Section 3.4): chunk compute tasks and
+ * the step planner.  Each Q partition of the tile is cut into k_Q chunks of
+ * P / k_Q rows and each KV partition into k_KV chunks of P / k_KV rows along
+ * the sequence; the chunk collectives AG-Q-i, AG-KV-j and RS-Q-i replace the
+ * whole-tile all-gathers and reduce-scatter, and compute task C-i-j attends
+ * Q chunk i of every Q partition to KV chunk j of every KV partition.
+ * ------------------------------------------------------------------------- */
+
+typedef struct {
+  int32_t q_chunk;       /* i in [0, num_q_chunks)                           */
+  int32_t num_q_chunks;  /* k_Q >= 1; P / k_Q a multiple of the Q block rows */
+  int32_t kv_chunk;      /* j in [0, num_kv_chunks)                          */
+  int32_t num_kv_chunks; /* k_KV >= 1; P / k_KV a multiple of the KV block
+                            rows (see mesh_attn_block_shape, pass 0)         */
+} ma_chunk_t;
+
+/* Device workspace bytes mesh_attn_chunk_fwd needs (any chunk of the tile). */
+size_t mesh_attn_chunk_fwd_workspace_size(const ma_problem_t* prob,
+                                          int32_t nq, int32_t nkv);
+
+/* Compute task C-i-j of the tile, as a running partial.
+ *   q     [nq*P/k_Q][Hq][d] bf16 device: chunk i of every Q partition in q_idx
+ *         order (the buffer AG-Q-i produces; row a*P/k_Q + r is local row
+ *         i*P/k_Q + r of partition q_idx[a]).
+ *   k, v  [nkv*P/k_KV][Hkv][d] bf16 device: chunk j of every KV partition in
+ *         kv_idx order (the buffer AG-KV-j produces).
+ *   o     [nq*P/k_Q][Hq][d] float32 device;  lse [Hq][nq*P/k_Q] float32.
+ *   accumulate  0: write the (O, LSE) of this chunk pair (O = 0, LSE = -inf
+ *               for a row that sees no key of it);
+ *               1: fold it into the (O, LSE) already in o, lse with the
+ *               online-softmax reducer (running accumulation over j), so
+ *               that after C-i-0 .. C-i-(k_KV-1) they hold Q chunk i's result
+ *               over the tile's whole KV footprint, ready for RS-Q-i.
+ * Positions, the causal rule and the layout are those of the whole problem:
+ * the result is exactly the tile's on these rows and keys.  Errors: as
+ * mesh_attn_tile_fwd, and MA_ERR_INVALID_ARG for a chunk outside its count or
+ * counts that do not divide P into whole blocks. */
+ma_status_t mesh_attn_chunk_fwd(const ma_problem_t* prob, const int32_t* q_idx,
+                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                                const ma_chunk_t* chunk, const void* q,
+                                const void* k, const void* v, float* o,
+                                float* lse, int32_t accumulate, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/* Kinds of the collective a GOO step runs. */
+enum { MA_GOO_NONE = 0, MA_GOO_AG_Q = 1, MA_GOO_AG_KV = 2, MA_GOO_RS_Q = 3 };
+
+typedef struct {
+  int32_t comm_kind;   /* MA_GOO_*; MA_GOO_NONE for a compute-only step     */
+  int32_t comm_chunk;  /* chunk index of the collective (-1 if none)        */
+  int32_t first_task;  /* this step's tasks are tasks[first_task ..         */
+  int32_t num_tasks;   /*   first_task + num_tasks) of the task list        */
+} ma_goo_step_t;
+
+/* Step-based greedy schedule of one tile's chunk tasks (host only,
+ * deterministic: every GPU of a mesh that calls it with the same shared costs
+ * gets the same collective order).  Each step runs one collective and the
+ * compute tasks listed for it, all ready when the step starts:
+ *   - its collective is, among the lowest-index chunk of each kind that can
+ *     run (RS-Q-i once every C-i-j is done), the one with the largest
+ *     (time of the compute it makes ready) / (its time); ties go to the one
+ *     that makes more compute ready, then to AG-KV, AG-Q, RS-Q in that order;
+ *   - its compute tasks are the ready ones in (i, j) order until their time
+ *     reaches gamma times the collective's time;
+ *   - when no collective can run, a compute-only step runs one ready task.
+ *   t_ag_q, t_ag_kv, t_rs_q  time of one chunk collective of each kind, > 0.
+ *   t_c         host [k_q][k_kv] float64, time of each C-i-j, >= 0.
+ *   steps       host array of max_steps entries (2 k_q + k_kv + k_q k_kv
+ *               always suffice); *num_steps receives the count.
+ *   tasks       host int32 [k_q * k_kv][2]: (i, j) in execution order.
+ * Errors: MA_ERR_INVALID_ARG for counts < 1 or k_q * k_kv > 4096, times that
+ * are not finite or not positive, NULL pointers; MA_ERR_CAPACITY if max_steps
+ * is too small. */
+ma_status_t mesh_attn_goo_plan(int32_t k_q, int32_t k_kv, double t_ag_q,
+                               double t_ag_kv, double t_rs_q,
+                               const double* t_c, double gamma,
+                               ma_goo_step_t* steps, int32_t max_steps,
+                               int32_t* tasks, int32_t* num_steps);
+
+/* ---------------------------------------------------------------------------
  * Online-softmax reducer (Section 2.2; the reducer of Algorithm 2's
  * reduce-scatter).  Folds k_parts partial results of the same rows over
  * disjoint key sets:  M = max_k lse_k,  lse = M + ln sum_k exp(lse_k - M),

@@ -27,5 +27,14 @@ from ._binding import (  # noqa: F401
     mesh_attn_tile_fwd,
     mesh_attn_lse_merge,
     mesh_attn_tile_bwd,
+    mesh_attn_chunk_fwd_workspace_size,
+    mesh_attn_chunk_fwd,
+    mesh_attn_goo_plan,
     mesh_attn_last_error,
+    Chunk,
+    GooStep,
+    MA_GOO_NONE,
+    MA_GOO_AG_Q,
+    MA_GOO_AG_KV,
+    MA_GOO_RS_Q,
 )

@@ -52,6 +52,26 @@ class Problem(ctypes.Structure):
 _lock = threading.Lock()
 _lib = None
 
+class Chunk(ctypes.Structure):
+    """ma_chunk_t: compute task C-i-j of a tile cut into k_Q x k_KV chunks."""
+    _fields_ = [("q_chunk", ctypes.c_int32),
+                ("num_q_chunks", ctypes.c_int32),
+                ("kv_chunk", ctypes.c_int32),
+                ("num_kv_chunks", ctypes.c_int32)]
+
+
+class GooStep(ctypes.Structure):
+    """ma_goo_step_t."""
+    _fields_ = [("comm_kind", ctypes.c_int32),
+                ("comm_chunk", ctypes.c_int32),
+                ("first_task", ctypes.c_int32),
+                ("num_tasks", ctypes.c_int32)]
+
+
+MA_GOO_NONE, MA_GOO_AG_Q, MA_GOO_AG_KV, MA_GOO_RS_Q = 0, 1, 2, 3
+GOO_KIND_NAMES = {MA_GOO_AG_Q: "AG-Q", MA_GOO_AG_KV: "AG-KV",
+                  MA_GOO_RS_Q: "RS-Q"}
+
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
 _p = ctypes.c_void_p
@@ -77,6 +97,15 @@ _SIGNATURES = {
                                    _i32, _p, _p]),
     "mesh_attn_tile_bwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _p, _p, _p,
                                   _p, _p, _p, _p, _p, _p, _i32, _p, _sz, _p]),
+    "mesh_attn_chunk_fwd_workspace_size": (_sz, [_PROB, _i32, _i32]),
+    "mesh_attn_chunk_fwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32,
+                                   ctypes.POINTER(Chunk), _p, _p, _p, _p, _p,
+                                   _i32, _p, _sz, _p]),
+    "mesh_attn_goo_plan": (_i32, [_i32, _i32, ctypes.c_double, ctypes.c_double,
+                                  ctypes.c_double,
+                                  ctypes.POINTER(ctypes.c_double),
+                                  ctypes.c_double, ctypes.POINTER(GooStep),
+                                  _i32, _I32P, _I32P]),
     "mesh_attn_last_error": (ctypes.c_char_p, []),
 }
 
@@ -310,3 +339,74 @@ def mesh_attn_tile_bwd(prob, q_idx, kv_idx, q, k, v, o, d_o, lse, dq, dk, dv,
         ctypes.c_void_p(ws.data_ptr()), wsb, _stream_ptr(stream))
     _check("mesh_attn_tile_bwd", st)
     return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# GOO (Section 3.4): chunk compute tasks and the step planner
+# ---------------------------------------------------------------------------
+
+def mesh_attn_chunk_fwd_workspace_size(prob, nq, nkv):
+    return int(load_library().mesh_attn_chunk_fwd_workspace_size(
+        ctypes.byref(Problem.make(prob)), int(nq), int(nkv)))
+
+
+def mesh_attn_chunk_fwd(prob, q_idx, kv_idx, chunk, q, k, v, o, lse,
+                        accumulate=0, ws=None, stream=None):
+    """Compute task C-i-j, ``chunk = (i, k_q, j, k_kv)``: ``q`` holds chunk i
+    of every Q partition, ``k, v`` chunk j of every KV partition; ``o``
+    (float32) and ``lse`` receive, or with ``accumulate=1`` fold in, the
+    chunk pair's partial."""
+    torch = _torch()
+    pr = Problem.make(prob)
+    qa, qp, nq = _idx(q_idx)
+    ka, kp, nkv = _idx(kv_idx)
+    ch = Chunk(*(int(x) for x in chunk))
+    P, hq, hkv, d = (pr.partition_len, pr.num_q_heads, pr.num_kv_heads,
+                     pr.head_dim)
+    if ch.num_q_chunks < 1 or ch.num_kv_chunks < 1:
+        raise ValueError("chunk counts must be >= 1")
+    rq, rk = nq * (P // ch.num_q_chunks), nkv * (P // ch.num_kv_chunks)
+    bf, f32 = (torch.bfloat16,), (torch.float32,)
+    args = [
+        _dev(q, "q", (rq, hq, d), bf),
+        _dev(k, "k", (rk, hkv, d), bf),
+        _dev(v, "v", (rk, hkv, d), bf),
+        _dev(o, "o", (rq, hq, d), f32),
+        _dev(lse, "lse", (hq, rq), f32),
+    ]
+    need = mesh_attn_chunk_fwd_workspace_size(pr, nq, nkv)
+    ws, wsb = _workspace(need, q.device, ws, stream)
+    st = load_library().mesh_attn_chunk_fwd(
+        ctypes.byref(pr), qp, nq, kp, nkv, ctypes.byref(ch), *args,
+        int(accumulate), ctypes.c_void_p(ws.data_ptr()), wsb,
+        _stream_ptr(stream))
+    _check("mesh_attn_chunk_fwd", st)
+    return o, lse
+
+
+def mesh_attn_goo_plan(k_q, k_kv, t_ag_q, t_ag_kv, t_rs_q, t_c, gamma=1.05):
+    """Greedy step schedule of a tile's chunk tasks.  Returns a list of steps
+    ``(comm, tasks)``: ``comm`` is ``None`` for a compute-only step, else
+    ``(kind, chunk)`` with kind "AG-Q", "AG-KV" or "RS-Q"; ``tasks`` is a list
+    of ``(i, j)``."""
+    k_q, k_kv = int(k_q), int(k_kv)
+    tc = np.ascontiguousarray(np.asarray(t_c, dtype=np.float64))
+    if tc.shape != (k_q, k_kv):
+        raise ValueError(f"t_c shape {tc.shape} != ({k_q}, {k_kv})")
+    max_steps = 2 * k_q + k_kv + k_q * k_kv
+    steps = (GooStep * max_steps)()
+    tasks = np.zeros((k_q * k_kv, 2), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    st = load_library().mesh_attn_goo_plan(
+        k_q, k_kv, float(t_ag_q), float(t_ag_kv), float(t_rs_q),
+        tc.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), float(gamma),
+        steps, max_steps, tasks.ctypes.data_as(_I32P), ctypes.byref(n))
+    _check("mesh_attn_goo_plan", st)
+    out = []
+    for s_ in steps[:n.value]:
+        comm = (None if s_.comm_kind == MA_GOO_NONE
+                else (GOO_KIND_NAMES[s_.comm_kind], int(s_.comm_chunk)))
+        out.append((comm, [tuple(int(x) for x in tasks[t])
+                           for t in range(s_.first_task,
+                                          s_.first_task + s_.num_tasks)]))
+    return out

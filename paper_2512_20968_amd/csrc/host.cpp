@@ -20,13 +20,17 @@
 #include <string>
 #include <vector>
 
+#include "host_error.h"
 #include "internal.h"
 
 using namespace mesh_attn;
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace mesh_attn {
+namespace host {
 
 ma_status_t fail(ma_status_t st, const char* fmt, ...) {
   char buf[512];
@@ -42,6 +46,14 @@ ma_status_t ok() {
   g_last_error.clear();
   return MA_OK;
 }
+
+}  // namespace host
+}  // namespace mesh_attn
+
+namespace {
+
+using mesh_attn::host::fail;
+using mesh_attn::host::ok;
 
 ma_status_t hip_fail(hipError_t e, const char* what) {
   return fail(MA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -149,16 +161,23 @@ struct Run {
   int32_t row, list, begin, end, cls;
 };
 
+// The rows of each partition a buffer holds: `len` consecutive local rows
+// starting at local row `off` (the whole partition, or one GOO chunk of it).
+struct Slice {
+  int64_t len, off;
+};
+
 // Runs of one orientation.  "Rows" are the blocks of side A (bm_a rows each,
 // lists a_idx), walked in buffer order; for each row, every list entry of side
 // B (blocks of bm_b) yields maximal equal-class runs, EMPTY dropped.  When
-// a_is_q, side A is the query side.
+// a_is_q, side A is the query side.  Each side's buffer holds slice sa / sb of
+// each of its partitions.
 void build_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
-                int32_t bm_a, const int32_t* b_idx, int32_t nb, int32_t bm_b,
-                bool a_is_q, std::vector<int32_t>* ptr, std::vector<Run>* runs) {
-  const int64_t P = p->partition_len;
-  const int32_t nab = static_cast<int32_t>(P / bm_a);
-  const int32_t nbb = static_cast<int32_t>(P / bm_b);
+                int32_t bm_a, Slice sa, const int32_t* b_idx, int32_t nb,
+                int32_t bm_b, Slice sb, bool a_is_q, std::vector<int32_t>* ptr,
+                std::vector<Run>* runs) {
+  const int32_t nab = static_cast<int32_t>(sa.len / bm_a);
+  const int32_t nbb = static_cast<int32_t>(sb.len / bm_b);
   const bool causal = p->causal != 0;
   ptr->assign(static_cast<size_t>(na) * nab + 1, 0);
   runs->clear();
@@ -166,17 +185,17 @@ void build_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
     for (int32_t ab = 0; ab < nab; ++ab) {
       const int32_t row = a * nab + ab;
       (*ptr)[row] = static_cast<int32_t>(runs->size());
-      const int64_t a_first = token_pos(p, a_idx[a], int64_t{ab} * bm_a);
-      const int64_t a_last =
-          token_pos(p, a_idx[a], int64_t{ab} * bm_a + bm_a - 1);
+      const int64_t a_row = sa.off + int64_t{ab} * bm_a;
+      const int64_t a_first = token_pos(p, a_idx[a], a_row);
+      const int64_t a_last = token_pos(p, a_idx[a], a_row + bm_a - 1);
       for (int32_t b = 0; b < nb; ++b) {
         int32_t kb = 0, cur = -1, start = 0;
         for (; kb <= nbb; ++kb) {
           int c = -2;
           if (kb < nbb) {
-            const int64_t b_first = token_pos(p, b_idx[b], int64_t{kb} * bm_b);
-            const int64_t b_last =
-                token_pos(p, b_idx[b], int64_t{kb} * bm_b + bm_b - 1);
+            const int64_t b_row = sb.off + int64_t{kb} * bm_b;
+            const int64_t b_first = token_pos(p, b_idx[b], b_row);
+            const int64_t b_last = token_pos(p, b_idx[b], b_row + bm_b - 1);
             c = a_is_q ? block_class(a_first, a_last, b_first, b_last, causal)
                        : block_class(b_first, b_last, a_first, a_last, causal);
           }
@@ -240,12 +259,14 @@ std::map<std::string, std::shared_ptr<Plan>> g_plans;
 constexpr size_t kMaxPlans = 1024;
 
 std::string plan_key(int pass, const ma_problem_t* p, const int32_t* q_idx,
-                     int32_t nq, const int32_t* kv_idx, int32_t nkv) {
+                     int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                     const ma_chunk_t& ch) {
   std::string k;
   auto put = [&k](const void* d, size_t n) {
     k.append(static_cast<const char*>(d), n);
   };
   put(&pass, sizeof pass);
+  put(&ch, sizeof ch);
   put(&p->num_partitions, sizeof(int32_t));
   put(&p->partition_len, sizeof(int32_t));
   put(&p->num_q_heads, sizeof(int32_t));
@@ -263,22 +284,21 @@ std::string plan_key(int pass, const ma_problem_t* p, const int32_t* q_idx,
 // workgroups; side B blocks (bm_b rows) are iterated.  delta = mask offset of
 // the query block/run against the key block/run (mask_offset).
 void device_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
-                 int32_t bm_a, const int32_t* b_idx, int32_t nb, int32_t bm_b,
-                 bool a_is_q, std::vector<int32_t>* ptr,
+                 int32_t bm_a, Slice sa, const int32_t* b_idx, int32_t nb,
+                 int32_t bm_b, Slice sb, bool a_is_q, std::vector<int32_t>* ptr,
                  std::vector<DevRun>* out, std::vector<int64_t>* work) {
   std::vector<Run> runs;
-  build_runs(p, a_idx, na, bm_a, b_idx, nb, bm_b, a_is_q, ptr, &runs);
-  const int64_t P = p->partition_len;
-  const int32_t nab = static_cast<int32_t>(P / bm_a);
-  const int32_t nbb = static_cast<int32_t>(P / bm_b);
+  build_runs(p, a_idx, na, bm_a, sa, b_idx, nb, bm_b, sb, a_is_q, ptr, &runs);
+  const int32_t nab = static_cast<int32_t>(sa.len / bm_a);
+  const int32_t nbb = static_cast<int32_t>(sb.len / bm_b);
   out->resize(runs.size());
   work->assign(ptr->size() - 1, 0);
   for (size_t i = 0; i < runs.size(); ++i) {
     const Run& r = runs[i];
     const int32_t a_part = a_idx[r.row / nab];
-    const int64_t a_row0 = int64_t{r.row % nab} * bm_a;
+    const int64_t a_row0 = sa.off + int64_t{r.row % nab} * bm_a;
     const int32_t b_part = b_idx[r.list];
-    const int64_t b_row0 = int64_t{r.begin} * bm_b;
+    const int64_t b_row0 = sb.off + int64_t{r.begin} * bm_b;
     const int64_t delta = a_is_q ? mask_offset(p, a_part, a_row0, b_part, b_row0)
                                  : mask_offset(p, b_part, b_row0, a_part, a_row0);
     (*out)[i] = DevRun{r.list * nbb + r.begin, r.end - r.begin, r.cls,
@@ -363,10 +383,15 @@ size_t side_bound(int64_t n_blocks, int64_t n_list, int64_t heads) {
          align_up((n_blocks * heads + kNumXcd) * sizeof(int2));
 }
 
+constexpr ma_chunk_t kWholeTile{0, 1, 0, 1};
+
 ma_status_t get_plan(int pass, const ma_problem_t* p, const int32_t* q_idx,
                      int32_t nq, const int32_t* kv_idx, int32_t nkv,
-                     std::shared_ptr<Plan>* out) {
-  const std::string key = plan_key(pass, p, q_idx, nq, kv_idx, nkv);
+                     const ma_chunk_t& ch, std::shared_ptr<Plan>* out) {
+  const std::string key = plan_key(pass, p, q_idx, nq, kv_idx, nkv, ch);
+  const int64_t P = p->partition_len;
+  const Slice sq{P / ch.num_q_chunks, ch.q_chunk * (P / ch.num_q_chunks)};
+  const Slice skv{P / ch.num_kv_chunks, ch.kv_chunk * (P / ch.num_kv_chunks)};
   std::lock_guard<std::mutex> lock(g_plan_mu);
   auto it = g_plans.find(key);
   if (it != g_plans.end()) {
@@ -377,15 +402,15 @@ ma_status_t get_plan(int pass, const ma_problem_t* p, const int32_t* q_idx,
   SideData sa, sb;
   std::vector<int64_t> work;
   if (pass == 0) {
-    device_runs(p, q_idx, nq, kFwdBM, kv_idx, nkv, kFwdBN, true, &sa.ptr,
-                &sa.runs, &work);
+    device_runs(p, q_idx, nq, kFwdBM, sq, kv_idx, nkv, kFwdBN, skv, true,
+                &sa.ptr, &sa.runs, &work);
     sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
   } else {
-    device_runs(p, q_idx, nq, kBwdBM, kv_idx, nkv, kBwdBN, true, &sa.ptr,
-                &sa.runs, &work);
+    device_runs(p, q_idx, nq, kBwdBM, sq, kv_idx, nkv, kBwdBN, skv, true,
+                &sa.ptr, &sa.runs, &work);
     sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
-    device_runs(p, kv_idx, nkv, kBwdBN, q_idx, nq, kBwdBM, false, &sb.ptr,
-                &sb.runs, &work);
+    device_runs(p, kv_idx, nkv, kBwdBN, skv, q_idx, nq, kBwdBM, sq, false,
+                &sb.ptr, &sb.runs, &work);
     sb.order = workgroup_order(work, p->num_kv_heads, 1, p->num_kv_heads);
   }
   auto plan = std::make_shared<Plan>();
@@ -428,6 +453,77 @@ ma_status_t check_head_dim(const ma_problem_t* p) {
 }
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+ma_status_t check_chunk(const ma_problem_t* p, const ma_chunk_t& c, int32_t bm,
+                        int32_t bn) {
+  if (c.num_q_chunks < 1 || c.num_kv_chunks < 1)
+    return fail(MA_ERR_INVALID_ARG, "chunk counts must be >= 1 (%d, %d)",
+                c.num_q_chunks, c.num_kv_chunks);
+  if (c.q_chunk < 0 || c.q_chunk >= c.num_q_chunks || c.kv_chunk < 0 ||
+      c.kv_chunk >= c.num_kv_chunks)
+    return fail(MA_ERR_INVALID_ARG, "chunk (%d of %d, %d of %d) out of range",
+                c.q_chunk, c.num_q_chunks, c.kv_chunk, c.num_kv_chunks);
+  const int64_t P = p->partition_len;
+  if (P % c.num_q_chunks != 0 || (P / c.num_q_chunks) % bm != 0 ||
+      P % c.num_kv_chunks != 0 || (P / c.num_kv_chunks) % bn != 0)
+    return fail(MA_ERR_INVALID_ARG,
+                "partition_len %lld must split into %d Q chunks of whole "
+                "%d-row blocks and %d KV chunks of whole %d-row blocks",
+                static_cast<long long>(P), c.num_q_chunks, bm,
+                c.num_kv_chunks, bn);
+  return MA_OK;
+}
+
+// Forward of one chunk pair of a tile (the whole tile: one chunk each).
+ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
+                     int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                     const ma_chunk_t& ch, const void* q, const void* k,
+                     const void* v, void* o, bool o_f32, float* lse,
+                     int32_t accumulate, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
+  if (st == MA_OK) st = check_head_dim(prob);
+  if (st == MA_OK) st = check_blocks(prob, kFwdBM, kFwdBN);
+  if (st == MA_OK) st = check_chunk(prob, ch, kFwdBM, kFwdBN);
+  if (st != MA_OK) return st;
+  const void* ptrs[] = {q, k, v, o, lse, ws};
+  const char* names[] = {"q", "k", "v", "o", "lse", "ws"};
+  for (int i = 0; i < 6; ++i) {
+    if (!ptrs[i]) return fail(MA_ERR_INVALID_ARG, "%s is NULL", names[i]);
+    if (!aligned16(ptrs[i]))
+      return fail(MA_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  }
+  const size_t need = fwd_ws_bound(prob, nq, nkv);
+  if (ws_bytes < need)
+    return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
+                ws_bytes, need);
+  std::shared_ptr<Plan> plan;
+  st = get_plan(0, prob, q_idx, nq, kv_idx, nkv, ch, &plan);
+  if (st != MA_OK) return st;
+  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
+                                hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
+  char* wsb = static_cast<char*>(ws);
+  FwdParams fp{};
+  fp.q = static_cast<const uint16_t*>(q);
+  fp.k = static_cast<const uint16_t*>(k);
+  fp.v = static_cast<const uint16_t*>(v);
+  fp.o = o;
+  fp.lse = lse;
+  fp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
+  fp.runs = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
+  fp.order = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
+  fp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
+  fp.hq = prob->num_q_heads;
+  fp.hkv = prob->num_kv_heads;
+  fp.group = prob->num_q_heads / prob->num_kv_heads;
+  fp.scale_log2 = prob->softmax_scale * kLog2e;
+  fp.accumulate = accumulate;
+  if (plan->a.grid == 0) return ok();  // cannot happen: every block is listed
+  e = launch_tile_fwd(fp, prob->head_dim, o_f32, plan->a.grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
+  return ok();
+}
 
 }  // namespace
 
@@ -486,7 +582,9 @@ ma_status_t mesh_attn_worklist(const ma_problem_t* prob, const int32_t* q_idx,
   if (st != MA_OK) return st;
   std::vector<int32_t> ptr;
   std::vector<Run> rl;
-  build_runs(prob, q_idx, nq, bm, kv_idx, nkv, bn, true, &ptr, &rl);
+  const Slice whole{prob->partition_len, 0};
+  build_runs(prob, q_idx, nq, bm, whole, kv_idx, nkv, bn, whole, true, &ptr,
+             &rl);
   return export_runs(ptr, rl, qblk_ptr, runs, cap, n_runs);
 }
 
@@ -501,7 +599,9 @@ ma_status_t mesh_attn_worklist_kv_major(const ma_problem_t* prob,
   if (st != MA_OK) return st;
   std::vector<int32_t> ptr;
   std::vector<Run> rl;
-  build_runs(prob, kv_idx, nkv, bn, q_idx, nq, bm, false, &ptr, &rl);
+  const Slice whole{prob->partition_len, 0};
+  build_runs(prob, kv_idx, nkv, bn, whole, q_idx, nq, bm, whole, false, &ptr,
+             &rl);
   return export_runs(ptr, rl, kvblk_ptr, runs, cap, n_runs);
 }
 
@@ -522,49 +622,30 @@ ma_status_t mesh_attn_tile_fwd(const ma_problem_t* prob, const int32_t* q_idx,
                                const void* q, const void* k, const void* v,
                                void* o, ma_dtype_t o_dtype, float* lse,
                                void* ws, size_t ws_bytes, hipStream_t stream) {
-  ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
-  if (st == MA_OK) st = check_head_dim(prob);
-  if (st == MA_OK) st = check_blocks(prob, kFwdBM, kFwdBN);
-  if (st != MA_OK) return st;
   if (o_dtype != MA_BF16 && o_dtype != MA_FP32)
     return fail(MA_ERR_INVALID_ARG, "o_dtype %d invalid", (int)o_dtype);
-  const void* ptrs[] = {q, k, v, o, lse, ws};
-  const char* names[] = {"q", "k", "v", "o", "lse", "ws"};
-  for (int i = 0; i < 6; ++i) {
-    if (!ptrs[i]) return fail(MA_ERR_INVALID_ARG, "%s is NULL", names[i]);
-    if (!aligned16(ptrs[i]))
-      return fail(MA_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
-  }
-  const size_t need = fwd_ws_bound(prob, nq, nkv);
-  if (ws_bytes < need)
-    return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
-                ws_bytes, need);
-  std::shared_ptr<Plan> plan;
-  st = get_plan(0, prob, q_idx, nq, kv_idx, nkv, &plan);
-  if (st != MA_OK) return st;
-  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
-                                hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
-  char* wsb = static_cast<char*>(ws);
-  FwdParams fp{};
-  fp.q = static_cast<const uint16_t*>(q);
-  fp.k = static_cast<const uint16_t*>(k);
-  fp.v = static_cast<const uint16_t*>(v);
-  fp.o = o;
-  fp.lse = lse;
-  fp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
-  fp.runs = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
-  fp.order = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
-  fp.rows_q = int64_t{nq} * prob->partition_len;
-  fp.hq = prob->num_q_heads;
-  fp.hkv = prob->num_kv_heads;
-  fp.group = prob->num_q_heads / prob->num_kv_heads;
-  fp.scale_log2 = prob->softmax_scale * kLog2e;
-  if (plan->a.grid == 0) return ok();  // cannot happen: every block is listed
-  e = launch_tile_fwd(fp, prob->head_dim, o_dtype == MA_FP32, plan->a.grid,
-                      stream);
-  if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
-  return ok();
+  return fwd_impl(prob, q_idx, nq, kv_idx, nkv, kWholeTile, q, k, v, o,
+                  o_dtype == MA_FP32, lse, 0, ws, ws_bytes, stream);
+}
+
+size_t mesh_attn_chunk_fwd_workspace_size(const ma_problem_t* prob,
+                                          int32_t nq, int32_t nkv) {
+  // A chunk's work list is never longer than the whole tile's.
+  return mesh_attn_fwd_workspace_size(prob, nq, nkv);
+}
+
+ma_status_t mesh_attn_chunk_fwd(const ma_problem_t* prob, const int32_t* q_idx,
+                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                                const ma_chunk_t* chunk, const void* q,
+                                const void* k, const void* v, float* o,
+                                float* lse, int32_t accumulate, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  if (!chunk) return fail(MA_ERR_INVALID_ARG, "chunk is NULL");
+  if (accumulate != 0 && accumulate != 1)
+    return fail(MA_ERR_INVALID_ARG, "accumulate must be 0 or 1, got %d",
+                accumulate);
+  return fwd_impl(prob, q_idx, nq, kv_idx, nkv, *chunk, q, k, v, o, true, lse,
+                  accumulate, ws, ws_bytes, stream);
 }
 
 ma_status_t mesh_attn_lse_merge(int32_t k_parts, int64_t rows, int32_t heads,
@@ -628,7 +709,7 @@ ma_status_t mesh_attn_tile_bwd(const ma_problem_t* prob, const int32_t* q_idx,
     return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
                 ws_bytes, need);
   std::shared_ptr<Plan> plan;
-  st = get_plan(1, prob, q_idx, nq, kv_idx, nkv, &plan);
+  st = get_plan(1, prob, q_idx, nq, kv_idx, nkv, kWholeTile, &plan);
   if (st != MA_OK) return st;
   hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
                                 hipMemcpyHostToDevice, stream);

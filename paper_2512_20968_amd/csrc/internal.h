@@ -41,6 +41,7 @@ struct FwdParams {
   int64_t rows_q;
   int32_t hq, hkv, group;
   float scale_log2;    // softmax scale * log2(e)
+  int32_t accumulate;  // 1: fold into the float32 (O, LSE) already stored
 };
 
 hipError_t launch_tile_fwd(const FwdParams& p, int head_dim, bool out_f32,

@@ -428,14 +428,37 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
   // Epilogue: O = acc / l, LSE = (m + log2 l) * ln 2.
   const float lt = l + __shfl_xor(l, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (lh == 0) {
-    const float lse = lt > 0.f ? (m + __builtin_amdgcn_logf(lt)) *
-                                     0.69314718055994531f
-                               : -INFINITY;
-    p.lse[int64_t{h} * p.rows_q + q_row] = lse;
+  const float lse2 = lt > 0.f ? m + __builtin_amdgcn_logf(lt) : -INFINITY;
+  const int64_t lidx = int64_t{h} * p.rows_q + q_row;
+  // Running accumulation (float32 partials only): fold (O, LSE) of this
+  // call into the stored pair with the two-part online-softmax reducer,
+  // lse = M + ln(e^(lse_old - M) + e^(lse_new - M)) with M the larger, and
+  // O = w_old O_old + w_new O_new with w = e^(lse_part - lse).  Both lane
+  // halves of a row read the stored LSE before the first half rewrites it
+  // (same wave, program order).
+  float w_old = 0.f, w_new = 1.f, lse_out = lse2;  // log2 units
+  if constexpr (OUT_F32) {
+    if (p.accumulate) {
+      const float old2 = p.lse[lidx] * 1.4426950408889634f;
+      const float mx = fmaxf(old2, lse2);
+      if (mx == -INFINITY) {
+        w_old = 1.f;  // neither part sees a key: keep the stored O = 0
+        w_new = 0.f;
+      } else {
+        const float a = exp2_fast(old2 - mx), b = exp2_fast(lse2 - mx);
+        const float sum = a + b;
+        lse_out = mx + __builtin_amdgcn_logf(sum);
+        w_old = a / sum;
+        w_new = b / sum;
+      }
+    }
   }
+  if (lh == 0)
+    p.lse[lidx] =
+        lse_out == -INFINITY ? -INFINITY : lse_out * 0.69314718055994531f;
   // O^T accumulator: register 4g+t of chunk cc holds dim 32cc + 8g + 4lh + t.
   const int64_t obase = (q_row * p.hq + h) * D;
+  const float sc_new = inv * w_new;
 #pragma unroll
   for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
@@ -443,9 +466,16 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
       const int dim = cc * 32 + g * 8 + lh * 4;
       f32x4 x;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) x[t] = oacc[cc][4 * g + t] * inv;
+      for (int t = 0; t < 4; ++t) x[t] = oacc[cc][4 * g + t] * sc_new;
       if constexpr (OUT_F32) {
-        *reinterpret_cast<f32x4*>(static_cast<float*>(p.o) + obase + dim) = x;
+        f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(p.o) + obase +
+                                              dim);
+        if (p.accumulate) {
+          const f32x4 prev = *dst;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) x[t] = fmaf(w_old, prev[t], x[t]);
+        }
+        *dst = x;
       } else {
         bf16x4 val;
 #pragma unroll

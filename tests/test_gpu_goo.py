@@ -1,0 +1,140 @@
+"""GPU parity of the GOO compute tasks (Section 3.4) through the C ABI: each
+chunk call C-i-j against the oracle's chunk task, and the running
+accumulation of C-i-0 .. C-i-(k_KV-1) against the oracle's (and the fused
+kernel's) whole tile on the rows of Q chunk i, in the planner's order."""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_20968_amd as ma
+from mesh_inputs import CONFIGS, make_qkv, sample_rows
+from oracle import goo
+
+from helpers import check_fwd, log, run_fwd, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _rows(P, n_parts, k, i, dev=None):
+    r = goo.chunk_buffer_rows(P, n_parts, k, i)
+    return torch.tensor(r, device=dev) if dev is not None else r
+
+
+def _run_chunks(cfg, qd, kd, vd, kq, kkv, order):
+    """Run every C-i-j in ``order`` (a list of (i, j)); the first task of each
+    Q chunk writes, the others accumulate.  Returns {i: (o, lse)}."""
+    P, hq, d = cfg.partition_len, cfg.num_q_heads, cfg.head_dim
+    prob = cfg.problem()
+    out = {}
+    qbuf = {i: qd[_rows(P, cfg.nq, kq, i, qd.device)].contiguous()
+            for i in range(kq)}
+    kbuf = {j: (kd[_rows(P, cfg.nkv, kkv, j, qd.device)].contiguous(),
+                vd[_rows(P, cfg.nkv, kkv, j, qd.device)].contiguous())
+            for j in range(kkv)}
+    for i, j in order:
+        first = i not in out
+        if first:
+            rq = cfg.nq * P // kq
+            out[i] = (torch.empty((rq, hq, d), dtype=torch.float32,
+                                  device=qd.device),
+                      torch.empty((hq, rq), dtype=torch.float32,
+                                  device=qd.device))
+        ma.mesh_attn_chunk_fwd(prob, cfg.q_idx, cfg.kv_idx, (i, kq, j, kkv),
+                               qbuf[i], kbuf[j][0], kbuf[j][1], out[i][0],
+                               out[i][1], accumulate=0 if first else 1)
+    return out
+
+
+def _small(layout, **kw):
+    base = dict(num_partitions=4, partition_len=1024, q_idx=[2, 3],
+                kv_idx=[0, 1, 2, 3], num_q_heads=4, num_kv_heads=2,
+                head_dim=128, causal=True, seed=51, layout=layout)
+    base.update(kw)
+    return dataclasses.replace(CONFIGS[1], **base)
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_single_chunk_task_matches_oracle(gpu, layout):
+    cfg = _small(layout)
+    q, k, v, _ = make_qkv(cfg)
+    P = cfg.partition_len
+    kq, kkv, i, j = 2, 4, 1, 2
+    qr, kr = _rows(P, cfg.nq, kq, i), _rows(P, cfg.nkv, kkv, j)
+    qd, kd, vd = (t.to(gpu) for t in (q[qr], k[kr], v[kr]))
+    o = torch.empty((len(qr), cfg.num_q_heads, cfg.head_dim),
+                    dtype=torch.float32, device=gpu)
+    lse = torch.empty((cfg.num_q_heads, len(qr)), dtype=torch.float32,
+                      device=gpu)
+    ma.mesh_attn_chunk_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx,
+                           (i, kq, j, kkv), qd, kd, vd, o, lse)
+    torch.cuda.synchronize()
+    ro, rl = goo.chunk_forward(cfg.problem(), cfg.q_idx, cfg.kv_idx, kq, i,
+                               kkv, j, to_np(q[qr]), to_np(k[kr]),
+                               to_np(v[kr]))
+    check_fwd(f"C-{i}-{j} layout={layout}", to_np(o), to_np(lse), ro, rl)
+
+
+@pytest.mark.parametrize("layout,kq,kkv", [(0, 2, 4), (1, 4, 2), (0, 1, 16),
+                                           (1, 4, 4)])
+def test_accumulated_chunks_equal_the_tile(gpu, layout, kq, kkv):
+    """All chunk tasks, in the GOO planner's order, accumulate to the tile:
+    every row against the oracle, and against the fused kernel."""
+    cfg = _small(layout)
+    q, k, v, _ = make_qkv(cfg)
+    qd, kd, vd = (t.to(gpu) for t in (q, k, v))
+    steps = ma.mesh_attn_goo_plan(kq, kkv, 0.5, 1.0, 0.5,
+                                  np.full((kq, kkv), 0.5), 1.05)
+    order = [t for _, tasks in steps for t in tasks]
+    assert sorted(order) == [(i, j) for i in range(kq) for j in range(kkv)]
+    out = _run_chunks(cfg, qd, kd, vd, kq, kkv, order)
+    fo, fl = run_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx, qd, kd, vd,
+                     torch.float32)
+    torch.cuda.synchronize()
+    ro, rl = oracle.tile_forward(cfg.problem(), cfg.q_idx, cfg.kv_idx,
+                                 to_np(q), to_np(k), to_np(v))
+    P = cfg.partition_len
+    for i in range(kq):
+        r = _rows(P, cfg.nq, kq, i)
+        tag = f"chunks {kq}x{kkv} layout={layout} Q chunk {i}"
+        check_fwd(tag, to_np(out[i][0]), to_np(out[i][1]), ro[r], rl[:, r])
+        # The fused kernel rounds P to bf16 against other running maxima, so
+        # the two agree to the forward tolerance, not bit for bit.
+        check_fwd(tag + " vs fused", to_np(out[i][0]), to_np(out[i][1]),
+                  to_np(fo)[r], to_np(fl)[:, r])
+
+
+def test_config2_in_4x4_chunk_tasks(gpu):
+    """The causal 64K tile as 16 chunk tasks: sampled rows against the
+    oracle, all rows against the fused kernel."""
+    cfg = CONFIGS[2]
+    kq = kkv = 4
+    q, k, v, _ = make_qkv(cfg)
+    qd, kd, vd = (t.to(gpu) for t in (q, k, v))
+    order = [(i, j) for i in range(kq) for j in range(kkv)]
+    log("config 2: 16 chunk tasks")
+    out = _run_chunks(cfg, qd, kd, vd, kq, kkv, order)
+    fo, fl = run_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx, qd, kd, vd,
+                     torch.float32)
+    torch.cuda.synchronize()
+    P = cfg.partition_len
+    o_all = torch.empty_like(fo)
+    l_all = torch.empty_like(fl)
+    for i in range(kq):
+        r = _rows(P, cfg.nq, kq, i, gpu)
+        o_all[r] = out[i][0]
+        l_all[:, r] = out[i][1]
+    check_fwd("config 2 as 4x4 chunks vs fused (all rows)", to_np(o_all),
+              to_np(l_all), to_np(fo).astype(np.float64),
+              to_np(fl).astype(np.float64))
+    rows = sample_rows(cfg, cfg.nq, n_random=16)
+    heads = [0, 9, 31]
+    ro, rl = oracle.tile_forward(cfg.problem(), cfg.q_idx, cfg.kv_idx,
+                                 to_np(q), to_np(k), to_np(v), rows=rows,
+                                 heads=heads)
+    rr = torch.tensor(rows, device=gpu)
+    check_fwd("config 2 as 4x4 chunks", to_np(o_all[rr][:, heads]),
+              to_np(l_all[heads][:, rr]), ro, rl)
