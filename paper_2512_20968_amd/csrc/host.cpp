@@ -442,7 +442,7 @@ size_t bwd_ws_bound(const ma_problem_t* p, int32_t nq, int32_t nkv) {
   const int64_t rows_q = int64_t{nq} * p->partition_len;
   return side_bound(nqb, nkv, p->num_q_heads) +
          side_bound(nkb, nq, p->num_kv_heads) +
-         align_up(static_cast<size_t>(rows_q) * p->num_q_heads * 4);
+         2 * align_up(static_cast<size_t>(rows_q) * p->num_q_heads * 4);
 }
 
 ma_status_t check_head_dim(const ma_problem_t* p) {
@@ -726,6 +726,10 @@ ma_status_t mesh_attn_tile_bwd(const ma_problem_t* prob, const int32_t* q_idx,
   bp.dk = dk;
   bp.dv = dv;
   bp.delta = reinterpret_cast<float*>(wsb + align_up(plan->bytes));
+  bp.lse2 = reinterpret_cast<float*>(
+      wsb + align_up(plan->bytes) +
+      align_up(static_cast<size_t>(nq) * prob->partition_len *
+               prob->num_q_heads * 4));
   bp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
   bp.qruns = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
   bp.qorder = reinterpret_cast<const int2*>(wsb + plan->a.off_order);

@@ -70,6 +70,7 @@ struct BwdParams {
   float* dk;
   float* dv;
   float* delta;        // workspace [hq][rows_q]: rowsum(dO * O)
+  float* lse2;         // workspace [hq][rows_q]: LSE * log2(e), -inf -> +inf
   // Q-major runs (dQ kernel): Q blocks of kBwdBM rows, KV blocks of kBwdBN.
   const int32_t* qblk_ptr;
   const DevRun* qruns;

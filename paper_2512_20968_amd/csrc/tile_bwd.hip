@@ -3,7 +3,9 @@
 // owned by exactly one thread, no atomics.
 //
 // Three launches on the caller's stream:
-//  1. delta:  D_i = <dO_i, O_i> for every (row, query head), float32.
+//  1. prep:   D_i = <dO_i, O_i> and LSE_i * log2(e) for every (row, query
+//     head), float32 (a row without a visible key gets +inf, so that its
+//     probabilities exp2(s S - LSE) are 0).
 //  2. dK/dV:  one workgroup per (KV block of 128 keys, KV head), 4 waves x 32
 //     keys.  It walks the KV block's runs of Q blocks (KV-major work list) for
 //     every query head of the GQA group, in 64-row stages, and keeps dK, dV
@@ -13,10 +15,16 @@
 //     32 rows, walking the Q-major runs of KV blocks in 64-key stages:
 //     S^T = K Q^T,  dP^T = V dO^T,  dS^T = P^T (dP^T - D),  dQ^T += s K^T dS^T.
 //
-// As in the forward, the operand that feeds a score tile is read in the
-// bit-2/3-swapped row order, so the probability / dS accumulators are already
-// k-contiguous operands of the next MFMA.  Tiles needed with k along rows
-// (Q, dO in dK/dV; K in dQ) are also stored transposed in LDS.
+// The stage tiles (Q and dO, or K and V: 64 rows x d) stream from HBM
+// straight into LDS (buffer loads with the LDS-destination form), double
+// buffered, one barrier per stage.  Each tile is stored once, row-major, and
+// read two ways: as rows (the A operand of the score MFMAs, 16-byte reads) and
+// transposed (the B operand of dV / dK, the A operand of dQ) through the
+// gfx950 LDS transpose read ds_read_b64_tr_b16.  One XOR swizzle of the
+// 16-byte chunks serves both access patterns without bank conflicts.  As in
+// the forward, the operand that feeds a score tile is read in the
+// bit-2/3-swapped row order, so the probability and dS accumulators are
+// already the k-contiguous operands of the next MFMA.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -29,19 +37,19 @@ namespace {
 
 using namespace dev;
 
-constexpr int NT = kThreads;
-constexpr int BQ = kBwdBM;    // 128
-constexpr int BK = kBwdBN;    // 128
+constexpr int NT = kThreads;    // 256: four waves
+constexpr int BQ = kBwdBM;      // 128
+constexpr int BK = kBwdBN;      // 128
 constexpr int SUB = kTileRows;  // 64 rows per LDS stage
 constexpr float kLog2e = 1.4426950408889634f;
 
 static_assert(BQ == 2 * SUB && BK == 2 * SUB, "two stages per block");
 
 // ---------------------------------------------------------------------------
-// 1. delta
+// 1. prep: delta and the log2-domain LSE
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(NT) void bwd_delta_kernel(BwdParams p) {
+__global__ __launch_bounds__(NT) void bwd_prep_kernel(BwdParams p) {
   constexpr int LPI = D / 8;  // lanes per (row, head)
   const int64_t gid = int64_t{blockIdx.x} * NT + threadIdx.x;
   const int64_t item = gid / LPI;  // row * hq + h
@@ -61,42 +69,142 @@ __global__ __launch_bounds__(NT) void bwd_delta_kernel(BwdParams p) {
   if (valid && sub == 0) {
     const int64_t row = item / p.hq;
     const int h = static_cast<int>(item - row * p.hq);
-    p.delta[int64_t{h} * p.rows_q + row] = s;
+    const int64_t idx = int64_t{h} * p.rows_q + row;
+    p.delta[idx] = s;
+    const float lse = p.lse[idx];
+    p.lse2[idx] = lse == -INFINITY ? INFINITY : lse * kLog2e;
   }
 }
 
-// Log2-domain LSE used to form P; a row without any visible key (LSE = -inf)
-// maps to +inf so that its probabilities are exp2(-inf) = 0.
-__device__ __forceinline__ float lse_log2(float lse) {
-  return lse == -INFINITY ? INFINITY : lse * kLog2e;
+// ---------------------------------------------------------------------------
+// Stage tiles: 64 rows x D bf16, row-major, 16-byte chunks XOR-swizzled.
+// ---------------------------------------------------------------------------
+template <int D>
+struct StageTile {
+  static constexpr int ROWB = 2 * D;        // bytes per row
+  static constexpr int CPR = D / 8;         // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;      // rows per 1 KB wave load
+  static constexpr int RPW = SUB / 4;       // rows each wave loads (16)
+  static constexpr int NLD = RPW / RPI;     // loads per wave per tile
+  static constexpr int BYTES = SUB * ROWB;
+  // Physical chunk of logical chunk c in row r is c ^ swz(r).  Row reads (16
+  // lanes: 16 distinct rows, one chunk) need swz to be one-to-one on the 16
+  // rows of a group; transpose reads (32 lanes: 4 rows x 4 chunks, or for
+  // d = 64 two row pairs sharing the banks) need the rows of a quad to land
+  // in different 4-chunk groups.  Both hold for these maps.
+  __device__ static int swz(int r) {
+    return D == 128 ? 4 * (r & 3) + ((r >> 2) & 3)
+                    : 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
+  }
+};
+
+// Per-lane byte offsets into a stage tile.
+template <int D>
+struct TileAddr {
+  using T = StageTile<D>;
+  uint32_t load;   // load j: lane's global offset within the rows of load j
+  int row;         // row reads: row perm(li) (+32 t), chunk 2kk + lh
+  int tr0, tr1;    // transpose reads, first and second half (+4 rows)
+
+  __device__ void init(int lane, int wg, uint32_t row_bytes_g) {
+    const int li = lane & 31, lh = lane >> 5;
+    {
+      const int r = mfma_row_perm(li);
+      row = r * T::ROWB + ((lh ^ T::swz(r)) * 16);
+    }
+    {
+      // ds_read_b64_tr_b16: in 16-lane group g, lane s supplies row
+      // 8*(g>>1) + s/4 (+4 for the second half, +16 per key step) at columns
+      // 16*(g&1) + 4*(s%4) .. +3 of a 32-column chunk; lane l then holds
+      // column l%32 of 8 consecutive rows (4 per half).
+      const int g16 = lane >> 4, s16 = lane & 15;
+      const int c16 = 2 * (g16 & 1) + ((s16 & 3) >> 1);
+      const int r0 = 8 * (g16 >> 1) + (s16 >> 2);
+      tr0 = r0 * T::ROWB + ((c16 ^ T::swz(r0)) * 16) + 8 * (s16 & 1);
+      const int r1 = r0 + 4;
+      tr1 = r1 * T::ROWB + ((c16 ^ T::swz(r1)) * 16) + 8 * (s16 & 1);
+    }
+    (void)wg;
+    (void)row_bytes_g;
+  }
+};
+
+// Rows [row0, row0 + 64) of one head of a [rows][heads][D] bf16 tensor into a
+// stage tile; each of the four waves loads 16 rows (NLD loads of 1 KB).  Lane
+// i of load j fills row wg*16 + j*RPI + i/CPR, physical chunk i%CPR, i.e.
+// logical chunk (i%CPR) ^ swz(row).
+template <int D>
+__device__ __forceinline__ void load_stage_tile(const uint16_t* base,
+                                                int64_t row0, int heads,
+                                                int head, char* tile, int wg,
+                                                int lane) {
+  using T = StageTile<D>;
+  const uint32_t row_bytes_g = static_cast<uint32_t>(heads) * D * 2;
+  const rsrc_t r = make_rsrc(base + (row0 * heads + head) * D,
+                             static_cast<uint32_t>(SUB) * row_bytes_g);
+  const int lrow = lane / T::CPR, lchunk = lane % T::CPR;
+#pragma unroll
+  for (int j = 0; j < T::NLD; ++j) {
+    const int tr = wg * T::RPW + j * T::RPI;  // first row of this load
+    const uint32_t voff =
+        lrow * row_bytes_g + ((lchunk ^ T::swz(tr + lrow)) * 16);
+    buffer_load16_lds(r, tile + tr * T::ROWB, voff, tr * row_bytes_g);
+  }
+}
+
+// 64 floats (one stage's rows of one head) into LDS, by one wave.
+__device__ __forceinline__ void load_stage_floats(const float* src,
+                                                  float* dst, int lane) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  const rsrc_t r = make_rsrc(src, SUB * 4);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst), 4, lane * 4,
+                                           0, 0, 0);
+}
+
+// A operand: rows perm(li) + 32*t of a tile, dims 16*kk + 8*lh .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 read_row_op(const char* tile, int addr,
+                                              int t, int kk) {
+  return *reinterpret_cast<const bf16x8*>(
+      tile + (addr ^ (32 * kk)) + t * 32 * StageTile<D>::ROWB);
+}
+
+// Transposed operand: column 32*cc + l%32 of rows 16*ss + 8*lh .. +7.
+template <int D>
+__device__ __forceinline__ bf16x8 read_tr_op(const char* tile,
+                                             const TileAddr<D>& a, int cc,
+                                             int ss) {
+  const char* b = tile + ss * 16 * StageTile<D>::ROWB;
+  return join_bf16(lds_read_tr16(b + (a.tr0 ^ (64 * cc))),
+                   lds_read_tr16(b + (a.tr1 ^ (64 * cc))));
 }
 
 // ---------------------------------------------------------------------------
 // 2. dK / dV
 // ---------------------------------------------------------------------------
 template <int D>
-struct DkdvStage {
-  static constexpr int TILE = SUB * D;          // bf16 elements per tile
-  static constexpr int FLOATS = 2 * SUB;        // lse2 + delta
-  static constexpr int ELEMS = 4 * TILE + 2 * FLOATS;  // in uint16 units
+struct DkdvLayout {
+  static constexpr int TILE = StageTile<D>::BYTES;
+  static constexpr int STAGE = 2 * TILE + 2 * SUB * 4;  // Q, dO, lse2, delta
+  static constexpr int SMEM = 2 * STAGE;
 };
 
 template <int D>
 __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
-  extern __shared__ __align__(16) uint16_t smem[];
-  using S = DkdvStage<D>;
+  extern __shared__ __align__(16) char smem[];
+  using L = DkdvLayout<D>;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  const int2 item = p.kvorder[blockIdx.x];
+  const int2 item = load_const(p.kvorder, blockIdx.x);
   if (item.x < 0) return;
   const int kvblk = item.x;
   const int hk = item.y;
-  const int run_b = p.kvblk_ptr[kvblk];
-  const int run_e = p.kvblk_ptr[kvblk + 1];
+  const int run_b = load_const(p.kvblk_ptr, kvblk);
+  const int run_e = load_const(p.kvblk_ptr, kvblk + 1);
   const int k_in_blk = wave * 32 + li;
   const int64_t kv_row = int64_t{kvblk} * BK + k_in_blk;
 
@@ -112,129 +220,151 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   }
 
   if (run_b < run_e) {
-    RowTile<D> tq, tdo;
-    float lse_v = 0.f, dlt_v = 0.f;
-    // Cursor over (query head of the group, run, block in run, stage).
-    int g = 0, r = run_b, off = 0, s = 0;
-    DevRun cur = p.kvruns[r];
-
-    auto load = [&](const DevRun& rn, int gg, int of, int st) {
-      const int h = hk * p.group + gg;
-      const int64_t row0 = int64_t{rn.blk0 + of} * BQ + st * SUB;
-      tq.load(p.q, row0, p.hq, h, tid);
-      tdo.load(p.d_o, row0, p.hq, h, tid);
-      if (tid < SUB) {
-        lse_v = lse_log2(p.lse[int64_t{h} * p.rows_q + row0 + tid]);
-        dlt_v = p.delta[int64_t{h} * p.rows_q + row0 + tid];
-      }
+    TileAddr<D> ta;
+    ta.init(lane, wave, 0);
+    // Stage cursor over (query head of the group, run, block in run, half).
+    struct Cur {
+      int g, r, off, s;
+      DevRun run;
     };
-    auto store = [&](int stage) {
-      uint16_t* base = smem + stage * S::ELEMS;
-      tq.store_rows(base, tid);
-      tq.store_cols(base + S::TILE, tid);
-      tdo.store_rows(base + 2 * S::TILE, tid);
-      tdo.store_cols(base + 3 * S::TILE, tid);
-      if (tid < SUB) {
-        float* f = reinterpret_cast<float*>(base + 4 * S::TILE);
-        f[tid] = lse_v;
-        f[SUB + tid] = dlt_v;
-      }
+    auto first = [&]() {
+      Cur c{0, run_b, 0, 0, load_const(p.kvruns, run_b)};
+      return c;
     };
-
-    load(cur, g, off, s);
-    store(0);
-    __syncthreads();
-    int stage = 0;
-    while (true) {
-      int ng = g, nr = r, noff = off, ns = s + 1;
-      if (ns == 2) {
-        ns = 0;
-        if (++noff == cur.nblk) {
-          noff = 0;
-          if (++nr == run_e) {
-            nr = run_b;
-            ++ng;
+    auto advance = [&](Cur c, bool* valid) {
+      if (++c.s == 2) {
+        c.s = 0;
+        if (++c.off == c.run.nblk) {
+          c.off = 0;
+          if (++c.r == run_e) {
+            c.r = run_b;
+            ++c.g;
           }
+          c.run = load_const(p.kvruns, c.r);
         }
       }
-      const bool has_next = ng < p.group;
-      DevRun nxt = cur;
-      if (has_next) {
-        nxt = p.kvruns[nr];
-        load(nxt, ng, noff, ns);
-      }
+      *valid = c.g < p.group;
+      return c;
+    };
+    auto issue = [&](const Cur& c, int buf) {
+      char* base = smem + buf * L::STAGE;
+      const int h = hk * p.group + c.g;
+      const int64_t row0 = int64_t{c.run.blk0 + c.off} * BQ + c.s * SUB;
+      load_stage_tile<D>(p.q, row0, p.hq, h, base, wave, lane);
+      load_stage_tile<D>(p.d_o, row0, p.hq, h, base + L::TILE, wave, lane);
+      float* f = reinterpret_cast<float*>(base + 2 * L::TILE);
+      if (wave == 0) load_stage_floats(p.lse2 + int64_t{h} * p.rows_q + row0,
+                                       f, lane);
+      if (wave == 1) load_stage_floats(p.delta + int64_t{h} * p.rows_q + row0,
+                                       f + SUB, lane);
+    };
 
-      const uint16_t* base = smem + stage * S::ELEMS;
-      const uint16_t* sq = base;
-      const uint16_t* sqt = base + S::TILE;
-      const uint16_t* sdo = base + 2 * S::TILE;
-      const uint16_t* sdot = base + 3 * S::TILE;
-      const float* slse = reinterpret_cast<const float*>(base + 4 * S::TILE);
+    Cur cur = first();
+    issue(cur, 0);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      wait_for(kf[kk]);
+      wait_for(vf[kk]);
+    }
+    wait_vmem();
+    __syncthreads();
+    int buf = 0;
+    while (true) {
+      bool has_next;
+      const Cur nxt = advance(cur, &has_next);
+      if (has_next) issue(nxt, buf ^ 1);
+
+      const char* base = smem + buf * L::STAGE;
+      const char* sq = base;
+      const char* sdo = base + L::TILE;
+      const float* slse = reinterpret_cast<const float*>(base + 2 * L::TILE);
       const float* sdlt = slse + SUB;
 
-      // S = Q K^T and dP = dO V^T for two 32-row query tiles; lane li owns
-      // key k_in_blk, register i owns query 32*qt + acc_row(i, lh).
-      f32x16 sc[2], dp[2];
+      // One 32-query tile at a time: S = Q K^T and dP = dO V^T (lane li owns
+      // key k_in_blk, register i owns query 32*qt + acc_row(i, lh)), then P
+      // and dS, then dV += P^T dO and dK += dS^T Q over those 32 queries
+      // (scale applied at the end; the B operands dO^T and Q^T are read
+      // transposed from the row tiles).
+      const int lim = k_in_blk - cur.run.delta - cur.off * BQ - cur.s * SUB;
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        zero(sc[qt]);
-        zero(dp[qt]);
-        const int row = qt * 32 + mfma_row_perm(li);
+        f32x16 sc, dp;
+        zero(sc);
+        zero(dp);
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) {
-          sc[qt] = mfma32(read_rows<D>(sq, row, kk, lh), kf[kk], sc[qt]);
-          dp[qt] = mfma32(read_rows<D>(sdo, row, kk, lh), vf[kk], dp[qt]);
+          sc = mfma32(read_row_op<D>(sq, ta.row, qt, kk), kf[kk], sc);
+          dp = mfma32(read_row_op<D>(sdo, ta.row, qt, kk), vf[kk], dp);
         }
-      }
-      if (cur.cls == 1) {
-        // key k of the block is hidden from query q of the run iff
-        // k - q > delta + (offset of this stage in the run).
-        const int lim = k_in_blk - cur.delta - off * BQ - s * SUB;
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i)
-            if (qt * 32 + acc_row(i, lh) < lim) sc[qt][i] = -INFINITY;
-      }
-      bf16x8 pb[4], dsb[4];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+        // LSE and D of this lane's 16 queries of the tile.
+        f32x4 lse4[2][2], dlt4[2][2];
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const int q0 = qt * 32 + hh * 16 + lh * 8;
-          const f32x4 l0 = *reinterpret_cast<const f32x4*>(slse + q0);
-          const f32x4 l1 = *reinterpret_cast<const f32x4*>(slse + q0 + 4);
-          const f32x4 d0 = *reinterpret_cast<const f32x4*>(sdlt + q0);
-          const f32x4 d1 = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4);
+#pragma unroll
+          for (int x = 0; x < 2; ++x) {
+            lse4[hh][x] = *reinterpret_cast<const f32x4*>(slse + q0 + 4 * x);
+            dlt4[hh][x] = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4 * x);
+          }
+        }
+        {
+          // One operand read per MFMA, three in flight; the 8 LSE / D reads
+          // go out with the last three MFMAs, so they are not held in
+          // registers across the whole phase.
+          constexpr int NM = D / 8;
+          __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+          for (int i = 0; i < NM - 3; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+        }
+        if (cur.run.cls == 1) {
+          // key k of the block is hidden from query q of the run iff
+          // k - q > delta + (offset of this stage in the run).
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if (qt * 32 + acc_row(i, lh) < lim) sc[i] = -INFINITY;
+        }
+        bf16x8 pb[2], dsb[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int i = hh * 8 + e;
-            const float lq = e < 4 ? l0[e] : l1[e - 4];
-            const float dq = e < 4 ? d0[e] : d1[e - 4];
-            const float pv = exp2_fast(fmaf(sc[qt][i], p.scale_log2, -lq));
-            pb[qt * 2 + hh][e] = static_cast<__bf16>(pv);
-            dsb[qt * 2 + hh][e] = static_cast<__bf16>(pv * (dp[qt][i] - dq));
+            const float lq = lse4[hh][e >> 2][e & 3];
+            const float dq = dlt4[hh][e >> 2][e & 3];
+            const float pv = exp2_fast(fmaf(sc[i], p.scale_log2, -lq));
+            pb[hh][e] = static_cast<__bf16>(pv);
+            dsb[hh][e] = static_cast<__bf16>(pv * (dp[i] - dq));
           }
-        }
-      // dV += P^T dO,  dK += dS^T Q   (scale applied at the end)
 #pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) {
-        const int dim = cc * 32 + li;
+        for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
-        for (int ss = 0; ss < 4; ++ss) {
-          dv[cc] = mfma32(pb[ss], read_cols(sdot, dim, ss, lh), dv[cc]);
-          dk[cc] = mfma32(dsb[ss], read_cols(sqt, dim, ss, lh), dk[cc]);
+          for (int hh = 0; hh < 2; ++hh) {
+            const int ss = 2 * qt + hh;
+            dv[cc] = mfma32(pb[hh], read_tr_op<D>(sdo, ta, cc, ss), dv[cc]);
+            dk[cc] = mfma32(dsb[hh], read_tr_op<D>(sq, ta, cc, ss), dk[cc]);
+          }
+        {
+          // Two transpose reads per MFMA, three MFMAs' worth in flight.
+          constexpr int NM = D / 8;
+          __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+          for (int i = 0; i < NM - 3; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
         }
       }
 
       if (!has_next) break;
-      store(stage ^ 1);
-      __syncthreads();
-      stage ^= 1;
-      g = ng;
-      r = nr;
-      off = noff;
-      s = ns;
+      wait_vmem();
+      lds_barrier();  // stage buf^1 landed; every wave is done with buf
+      buf ^= 1;
       cur = nxt;
     }
   }
@@ -263,30 +393,36 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
 // 3. dQ
 // ---------------------------------------------------------------------------
 template <int D>
+struct DqLayout {
+  static constexpr int TILE = StageTile<D>::BYTES;
+  static constexpr int STAGE = 2 * TILE;  // K, V
+  static constexpr int SMEM = 2 * STAGE;
+};
+
+template <int D>
 __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
-  extern __shared__ __align__(16) uint16_t smem[];
-  constexpr int TILE = SUB * D;
-  constexpr int ELEMS = 3 * TILE;  // K rows, K cols, V rows
+  extern __shared__ __align__(16) char smem[];
+  using L = DqLayout<D>;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  const int2 item = p.qorder[blockIdx.x];
+  const int2 item = load_const(p.qorder, blockIdx.x);
   if (item.x < 0) return;
   const int qblk = item.x;
   const int h = item.y;
   const int hk = h / p.group;
-  const int run_b = p.qblk_ptr[qblk];
-  const int run_e = p.qblk_ptr[qblk + 1];
+  const int run_b = load_const(p.qblk_ptr, qblk);
+  const int run_e = load_const(p.qblk_ptr, qblk + 1);
   const int q_in_blk = wave * 32 + li;
   const int64_t q_row = int64_t{qblk} * BQ + q_in_blk;
 
   bf16x8 qf[D / 16], dof[D / 16];
   load_frags<D>(qf, p.q, q_row, p.hq, h, lh);
   load_frags<D>(dof, p.d_o, q_row, p.hq, h, lh);
-  const float lse2 = lse_log2(p.lse[int64_t{h} * p.rows_q + q_row]);
+  const float lse2 = p.lse2[int64_t{h} * p.rows_q + q_row];
   const float dlt = p.delta[int64_t{h} * p.rows_q + q_row];
 
   f32x16 acc[D / 32];
@@ -294,44 +430,51 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
   for (int cc = 0; cc < D / 32; ++cc) zero(acc[cc]);
 
   if (run_b < run_e) {
-    RowTile<D> tk, tv;
-    int r = run_b, off = 0, s = 0;
-    DevRun cur = p.qruns[r];
-    auto load = [&](const DevRun& rn, int of, int st) {
-      const int64_t row0 = int64_t{rn.blk0 + of} * BK + st * SUB;
-      tk.load(p.k, row0, p.hkv, hk, tid);
-      tv.load(p.v, row0, p.hkv, hk, tid);
+    TileAddr<D> ta;
+    ta.init(lane, wave, 0);
+    struct Cur {
+      int r, off, s;
+      DevRun run;
     };
-    auto store = [&](int stage) {
-      uint16_t* base = smem + stage * ELEMS;
-      tk.store_rows(base, tid);
-      tk.store_cols(base + TILE, tid);
-      tv.store_rows(base + 2 * TILE, tid);
-    };
-    load(cur, off, s);
-    store(0);
-    __syncthreads();
-    int stage = 0;
-    while (true) {
-      int nr = r, noff = off, ns = s + 1;
-      if (ns == 2) {
-        ns = 0;
-        if (++noff == cur.nblk) {
-          noff = 0;
-          ++nr;
+    auto advance = [&](Cur c, bool* valid) {
+      *valid = true;
+      if (++c.s == 2) {
+        c.s = 0;
+        if (++c.off == c.run.nblk) {
+          c.off = 0;
+          if (++c.r == run_e)
+            *valid = false;
+          else
+            c.run = load_const(p.qruns, c.r);
         }
       }
-      const bool has_next = nr < run_e;
-      DevRun nxt = cur;
-      if (has_next) {
-        nxt = p.qruns[nr];
-        load(nxt, noff, ns);
-      }
+      return c;
+    };
+    auto issue = [&](const Cur& c, int buf) {
+      char* base = smem + buf * L::STAGE;
+      const int64_t row0 = int64_t{c.run.blk0 + c.off} * BK + c.s * SUB;
+      load_stage_tile<D>(p.k, row0, p.hkv, hk, base, wave, lane);
+      load_stage_tile<D>(p.v, row0, p.hkv, hk, base + L::TILE, wave, lane);
+    };
 
-      const uint16_t* base = smem + stage * ELEMS;
-      const uint16_t* sk = base;
-      const uint16_t* skt = base + TILE;
-      const uint16_t* sv = base + 2 * TILE;
+    Cur cur{run_b, 0, 0, load_const(p.qruns, run_b)};
+    issue(cur, 0);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      wait_for(qf[kk]);
+      wait_for(dof[kk]);
+    }
+    wait_vmem();
+    __syncthreads();
+    int buf = 0;
+    while (true) {
+      bool has_next;
+      const Cur nxt = advance(cur, &has_next);
+      if (has_next) issue(nxt, buf ^ 1);
+
+      const char* base = smem + buf * L::STAGE;
+      const char* sk = base;
+      const char* sv = base + L::TILE;
 
       // S^T = K Q^T, dP^T = V dO^T: lane li owns query q_in_blk, register i
       // owns key 32*kt + acc_row(i, lh) of the stage.
@@ -340,15 +483,24 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
       for (int kt = 0; kt < 2; ++kt) {
         zero(sc[kt]);
         zero(dp[kt]);
-        const int row = kt * 32 + mfma_row_perm(li);
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) {
-          sc[kt] = mfma32(read_rows<D>(sk, row, kk, lh), qf[kk], sc[kt]);
-          dp[kt] = mfma32(read_rows<D>(sv, row, kk, lh), dof[kk], dp[kt]);
+          sc[kt] = mfma32(read_row_op<D>(sk, ta.row, kt, kk), qf[kk], sc[kt]);
+          dp[kt] = mfma32(read_row_op<D>(sv, ta.row, kt, kk), dof[kk], dp[kt]);
         }
       }
-      if (cur.cls == 1) {
-        const int lim = cur.delta - off * BK - s * SUB + q_in_blk;
+      {
+        constexpr int NM = D / 4;  // one operand read per MFMA, 3 in flight
+        __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+        for (int i = 0; i < NM - 3; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+      }
+      if (cur.run.cls == 1) {
+        const int lim = cur.run.delta - cur.off * BK - cur.s * SUB + q_in_blk;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -364,22 +516,28 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
           const float pv = exp2_fast(fmaf(sc[kt][i], p.scale_log2, -lse2));
           dsb[ss][e] = static_cast<__bf16>(pv * (dp[kt][i] - dlt));
         }
-      // dQ^T += K^T dS^T
+      // dQ^T += K^T dS^T: the A operand K^T is read transposed from the K
+      // row tile.
 #pragma unroll
-      for (int cc = 0; cc < D / 32; ++cc) {
-        const int dim = cc * 32 + li;
+      for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
         for (int ss = 0; ss < 4; ++ss)
-          acc[cc] = mfma32(read_cols(skt, dim, ss, lh), dsb[ss], acc[cc]);
+          acc[cc] = mfma32(read_tr_op<D>(sk, ta, cc, ss), dsb[ss], acc[cc]);
+      {
+        constexpr int NM = D / 8;  // two transpose reads per MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+        for (int i = 0; i < NM - 3; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
       }
 
       if (!has_next) break;
-      store(stage ^ 1);
-      __syncthreads();
-      stage ^= 1;
-      r = nr;
-      off = noff;
-      s = ns;
+      wait_vmem();
+      lds_barrier();  // stage buf^1 landed; every wave is done with buf
+      buf ^= 1;
       cur = nxt;
     }
   }
@@ -410,8 +568,8 @@ hipError_t set_smem(K kern, size_t bytes) {
 template <int D>
 hipError_t launch(const BwdParams& p, int grid_q, int grid_kv,
                   hipStream_t stream) {
-  const size_t smem_kv = 2 * DkdvStage<D>::ELEMS * sizeof(uint16_t);
-  const size_t smem_q = 2 * 3 * SUB * D * sizeof(uint16_t);
+  const size_t smem_kv = DkdvLayout<D>::SMEM;
+  const size_t smem_q = DqLayout<D>::SMEM;
   static bool attr_done = false;  // benign race: idempotent attribute set
   if (!attr_done) {
     hipError_t e = set_smem(bwd_dkdv_kernel<D>, smem_kv);
@@ -419,10 +577,10 @@ hipError_t launch(const BwdParams& p, int grid_q, int grid_kv,
     if (e != hipSuccess) return e;
     attr_done = true;
   }
-  const int64_t delta_threads = p.rows_q * p.hq * (D / 8);
-  const int delta_grid = static_cast<int>((delta_threads + NT - 1) / NT);
-  hipLaunchKernelGGL(bwd_delta_kernel<D>, dim3(delta_grid), dim3(NT), 0,
-                     stream, p);
+  const int64_t prep_threads = p.rows_q * p.hq * (D / 8);
+  const int prep_grid = static_cast<int>((prep_threads + NT - 1) / NT);
+  hipLaunchKernelGGL(bwd_prep_kernel<D>, dim3(prep_grid), dim3(NT), 0, stream,
+                     p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (grid_kv > 0) {
