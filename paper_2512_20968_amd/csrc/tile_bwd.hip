@@ -84,8 +84,6 @@ struct StageTile {
   static constexpr int ROWB = 2 * D;        // bytes per row
   static constexpr int CPR = D / 8;         // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;      // rows per 1 KB wave load
-  static constexpr int RPW = SUB / 4;       // rows each wave loads (16)
-  static constexpr int NLD = RPW / RPI;     // loads per wave per tile
   static constexpr int BYTES = SUB * ROWB;
   // Physical chunk of logical chunk c in row r is c ^ swz(r).  Row reads (16
   // lanes: 16 distinct rows, one chunk) need swz to be one-to-one on the 16
@@ -130,22 +128,24 @@ struct TileAddr {
 };
 
 // Rows [row0, row0 + 64) of one head of a [rows][heads][D] bf16 tensor into a
-// stage tile; each of the four waves loads 16 rows (NLD loads of 1 KB).  Lane
-// i of load j fills row wg*16 + j*RPI + i/CPR, physical chunk i%CPR, i.e.
-// logical chunk (i%CPR) ^ swz(row).
-template <int D>
+// stage tile, shared by NW waves: wave wg loads rows wg*64/NW .. +64/NW with
+// 1 KB loads.  Lane i of load j fills row wg*64/NW + j*RPI + i/CPR, physical
+// chunk i%CPR, i.e. logical chunk (i%CPR) ^ swz(row).
+template <int D, int NW = 4>
 __device__ __forceinline__ void load_stage_tile(const uint16_t* base,
                                                 int64_t row0, int heads,
                                                 int head, char* tile, int wg,
                                                 int lane) {
   using T = StageTile<D>;
+  constexpr int RPW = SUB / NW;
+  static_assert(RPW % T::RPI == 0, "whole loads per wave");
   const uint32_t row_bytes_g = static_cast<uint32_t>(heads) * D * 2;
   const rsrc_t r = make_rsrc(base + (row0 * heads + head) * D,
                              static_cast<uint32_t>(SUB) * row_bytes_g);
   const int lrow = lane / T::CPR, lchunk = lane % T::CPR;
 #pragma unroll
-  for (int j = 0; j < T::NLD; ++j) {
-    const int tr = wg * T::RPW + j * T::RPI;  // first row of this load
+  for (int j = 0; j < RPW / T::RPI; ++j) {
+    const int tr = wg * RPW + j * T::RPI;  // first row of this load
     const uint32_t voff =
         lrow * row_bytes_g + ((lchunk ^ T::swz(tr + lrow)) * 16);
     buffer_load16_lds(r, tile + tr * T::ROWB, voff, tr * row_bytes_g);
@@ -189,35 +189,33 @@ struct DkdvLayout {
   static constexpr int SMEM = 2 * STAGE;
 };
 
-template <int D>
-__global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
-  extern __shared__ __align__(16) char smem[];
+constexpr int NT_KV = 512;  // dK/dV: eight waves
+
+// Eight waves in two roles over the same 128 keys (wave w: keys 32*(w%4) ..
+// +32): waves 0-3 accumulate dV (S, P, dV += P^T dO), waves 4-7 dK (S, dP,
+// dS, dK += dS^T Q).  S is computed by both roles (5 products per stage pair
+// instead of 4), but each wave then holds one accumulator and its operand
+// fragments in 256 registers, so two waves share each SIMD and one's MFMAs
+// run while the other works on its softmax; the fused one-wave-per-SIMD form
+// needs dK, dV, K and V fragments together and runs out of registers.
+template <int D, int ROLE>
+__device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
+                                          int kvblk, int hk, int run_b,
+                                          int run_e, int wave, int lane) {
   using L = DkdvLayout<D>;
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int lane = tid & 63;
   const int li = lane & 31;
   const int lh = lane >> 5;
-
-  const int2 item = load_const(p.kvorder, blockIdx.x);
-  if (item.x < 0) return;
-  const int kvblk = item.x;
-  const int hk = item.y;
-  const int run_b = load_const(p.kvblk_ptr, kvblk);
-  const int run_e = load_const(p.kvblk_ptr, kvblk + 1);
-  const int k_in_blk = wave * 32 + li;
+  const int kw = wave & 3;
+  const int k_in_blk = kw * 32 + li;
   const int64_t kv_row = int64_t{kvblk} * BK + k_in_blk;
 
   bf16x8 kf[D / 16], vf[D / 16];
   load_frags<D>(kf, p.k, kv_row, p.hkv, hk, lh);
-  load_frags<D>(vf, p.v, kv_row, p.hkv, hk, lh);
+  if constexpr (ROLE == 1) load_frags<D>(vf, p.v, kv_row, p.hkv, hk, lh);
 
-  f32x16 dk[D / 32], dv[D / 32];
+  f32x16 acc[D / 32];
 #pragma unroll
-  for (int cc = 0; cc < D / 32; ++cc) {
-    zero(dk[cc]);
-    zero(dv[cc]);
-  }
+  for (int cc = 0; cc < D / 32; ++cc) zero(acc[cc]);
 
   if (run_b < run_e) {
     TileAddr<D> ta;
@@ -226,10 +224,6 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
     struct Cur {
       int g, r, off, s;
       DevRun run;
-    };
-    auto first = [&]() {
-      Cur c{0, run_b, 0, 0, load_const(p.kvruns, run_b)};
-      return c;
     };
     auto advance = [&](Cur c, bool* valid) {
       if (++c.s == 2) {
@@ -250,8 +244,8 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
       char* base = smem + buf * L::STAGE;
       const int h = hk * p.group + c.g;
       const int64_t row0 = int64_t{c.run.blk0 + c.off} * BQ + c.s * SUB;
-      load_stage_tile<D>(p.q, row0, p.hq, h, base, wave, lane);
-      load_stage_tile<D>(p.d_o, row0, p.hq, h, base + L::TILE, wave, lane);
+      load_stage_tile<D, 8>(p.q, row0, p.hq, h, base, wave, lane);
+      load_stage_tile<D, 8>(p.d_o, row0, p.hq, h, base + L::TILE, wave, lane);
       float* f = reinterpret_cast<float*>(base + 2 * L::TILE);
       if (wave == 0) load_stage_floats(p.lse2 + int64_t{h} * p.rows_q + row0,
                                        f, lane);
@@ -259,12 +253,12 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
                                        f + SUB, lane);
     };
 
-    Cur cur = first();
+    Cur cur{0, run_b, 0, 0, load_const(p.kvruns, run_b)};
     issue(cur, 0);
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       wait_for(kf[kk]);
-      wait_for(vf[kk]);
+      if constexpr (ROLE == 1) wait_for(vf[kk]);
     }
     wait_vmem();
     __syncthreads();
@@ -279,46 +273,30 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
       const char* sdo = base + L::TILE;
       const float* slse = reinterpret_cast<const float*>(base + 2 * L::TILE);
       const float* sdlt = slse + SUB;
-
-      // One 32-query tile at a time: S = Q K^T and dP = dO V^T (lane li owns
-      // key k_in_blk, register i owns query 32*qt + acc_row(i, lh)), then P
-      // and dS, then dV += P^T dO and dK += dS^T Q over those 32 queries
-      // (scale applied at the end; the B operands dO^T and Q^T are read
-      // transposed from the row tiles).
       const int lim = k_in_blk - cur.run.delta - cur.off * BQ - cur.s * SUB;
+
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
+        // S = Q K^T (and for dK, dP = dO V^T) of 32 queries; lane li owns
+        // key k_in_blk, register i owns query 32*qt + acc_row(i, lh).
+        __builtin_amdgcn_sched_barrier(0);
         f32x16 sc, dp;
         zero(sc);
-        zero(dp);
+        if constexpr (ROLE == 1) zero(dp);
 #pragma unroll
         for (int kk = 0; kk < D / 16; ++kk) {
           sc = mfma32(read_row_op<D>(sq, ta.row, qt, kk), kf[kk], sc);
-          dp = mfma32(read_row_op<D>(sdo, ta.row, qt, kk), vf[kk], dp);
-        }
-        // LSE and D of this lane's 16 queries of the tile.
-        f32x4 lse4[2][2], dlt4[2][2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int q0 = qt * 32 + hh * 16 + lh * 8;
-#pragma unroll
-          for (int x = 0; x < 2; ++x) {
-            lse4[hh][x] = *reinterpret_cast<const f32x4*>(slse + q0 + 4 * x);
-            dlt4[hh][x] = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4 * x);
-          }
+          if constexpr (ROLE == 1)
+            dp = mfma32(read_row_op<D>(sdo, ta.row, qt, kk), vf[kk], dp);
         }
         {
-          // One operand read per MFMA, three in flight; the 8 LSE / D reads
-          // go out with the last three MFMAs, so they are not held in
-          // registers across the whole phase.
-          constexpr int NM = D / 8;
+          constexpr int NM = (ROLE == 1 ? 2 : 1) * D / 16;
           __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
 #pragma unroll
           for (int i = 0; i < NM - 3; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
           __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
         }
         if (cur.run.cls == 1) {
@@ -328,29 +306,44 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
           for (int i = 0; i < 16; ++i)
             if (qt * 32 + acc_row(i, lh) < lim) sc[i] = -INFINITY;
         }
-        bf16x8 pb[2], dsb[2];
+        bf16x8 op[2];  // P (dV) or dS (dK), k-contiguous per lane half
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
+        for (int hh = 0; hh < 2; ++hh) {
+          const int q0 = qt * 32 + hh * 16 + lh * 8;
+          const f32x4 l0 = *reinterpret_cast<const f32x4*>(slse + q0);
+          const f32x4 l1 = *reinterpret_cast<const f32x4*>(slse + q0 + 4);
+          f32x4 d0, d1;
+          if constexpr (ROLE == 1) {
+            d0 = *reinterpret_cast<const f32x4*>(sdlt + q0);
+            d1 = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4);
+          }
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int i = hh * 8 + e;
-            const float lq = lse4[hh][e >> 2][e & 3];
-            const float dq = dlt4[hh][e >> 2][e & 3];
+            const float lq = e < 4 ? l0[e] : l1[e - 4];
             const float pv = exp2_fast(fmaf(sc[i], p.scale_log2, -lq));
-            pb[hh][e] = static_cast<__bf16>(pv);
-            dsb[hh][e] = static_cast<__bf16>(pv * (dp[i] - dq));
+            if constexpr (ROLE == 0) {
+              op[hh][e] = static_cast<__bf16>(pv);
+            } else {
+              const float dq = e < 4 ? d0[e] : d1[e - 4];
+              op[hh][e] = static_cast<__bf16>(pv * (dp[i] - dq));
+            }
           }
+        }
+        // dV += P^T dO or dK += dS^T Q (scale at the end); the B operand is
+        // read transposed from the dO or Q row tile.  A scheduling region of
+        // its own, so that the read-ahead pattern below is not mixed with the
+        // VALU work above.
+        __builtin_amdgcn_sched_barrier(0);
+        const char* bt = ROLE == 0 ? sdo : sq;
 #pragma unroll
         for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int ss = 2 * qt + hh;
-            dv[cc] = mfma32(pb[hh], read_tr_op<D>(sdo, ta, cc, ss), dv[cc]);
-            dk[cc] = mfma32(dsb[hh], read_tr_op<D>(sq, ta, cc, ss), dk[cc]);
-          }
+          for (int hh = 0; hh < 2; ++hh)
+            acc[cc] = mfma32(op[hh], read_tr_op<D>(bt, ta, cc, 2 * qt + hh),
+                             acc[cc]);
         {
-          // Two transpose reads per MFMA, three MFMAs' worth in flight.
-          constexpr int NM = D / 8;
+          constexpr int NM = D / 16;  // two transpose reads per MFMA
           __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
           for (int i = 0; i < NM - 3; ++i) {
@@ -370,23 +363,38 @@ __global__ __launch_bounds__(NT, 1) void bwd_dkdv_kernel(BwdParams p) {
   }
 
   // Accumulator register i of chunk cc: key row 8*(i/4) + 4*lh + i%4 of the
-  // wave, dim 32*cc + li.
+  // wave's 32 keys, dim 32*cc + li.
+  float* out = ROLE == 0 ? p.dv : p.dk;
+  const float sc_out = ROLE == 0 ? 1.f : p.scale;
 #pragma unroll
   for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int64_t row =
-          int64_t{kvblk} * BK + wave * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
+          int64_t{kvblk} * BK + kw * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
       const int64_t idx = (row * p.hkv + hk) * D + cc * 32 + li;
-      float kv = dk[cc][i] * p.scale;
-      float vv = dv[cc][i];
-      if (p.accumulate) {
-        kv += p.dk[idx];
-        vv += p.dv[idx];
-      }
-      p.dk[idx] = kv;
-      p.dv[idx] = vv;
+      float x = acc[cc][i] * sc_out;
+      if (p.accumulate) x += out[idx];
+      out[idx] = x;
     }
+}
+
+template <int D>
+__global__ __launch_bounds__(NT_KV, 1) void bwd_dkdv_kernel(BwdParams p) {
+  extern __shared__ __align__(16) char smem[];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int2 item = load_const(p.kvorder, blockIdx.x);
+  if (item.x < 0) return;
+  const int kvblk = item.x;
+  const int hk = item.y;
+  const int run_b = load_const(p.kvblk_ptr, kvblk);
+  const int run_e = load_const(p.kvblk_ptr, kvblk + 1);
+  if (wave < 4)
+    dkdv_role<D, 0>(p, smem, kvblk, hk, run_b, run_e, wave, lane);
+  else
+    dkdv_role<D, 1>(p, smem, kvblk, hk, run_b, run_e, wave, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -584,7 +592,7 @@ hipError_t launch(const BwdParams& p, int grid_q, int grid_kv,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (grid_kv > 0) {
-    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(grid_kv), dim3(NT), smem_kv,
+    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(grid_kv), dim3(NT_KV), smem_kv,
                        stream, p);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
