@@ -161,3 +161,40 @@ def accumulate_partial(o_run, lse_run, o_new, lse_new):
         o[:, h], lse[h] = lse_merge(np.stack([o_run[:, h], o_new[:, h]]),
                                     np.stack([lse_run[h], lse_new[h]]))
     return o, lse
+
+
+def chunk_backward(prob, q_idx, kv_idx, k_q, i, k_kv, j, q, k, v, do):
+    """Backward of compute task C-i-j (Algorithm 3's per-pair loop on one
+    chunk pair).  ``q, do [nq*P, Hq, d]`` and ``k, v [nkv*P, Hkv, d]`` are the
+    whole tile's buffers: the final O and LSE of the Q chunk's rows are those
+    over every key of the tile (computed here), while the gradient terms run
+    over the rows of Q chunk i and the keys of KV chunk j only.  Returns
+    ``dq [rows of Q chunk i, Hq, d]`` and ``dk, dv [rows of KV chunk j, Hkv,
+    d]`` (dK, dV summed over the query heads of each KV head)."""
+    from .attention import attention_rows, attention_rows_bwd, q_head_to_kv_head
+    P = int(prob["partition_len"])
+    hq, hkv = int(prob["num_q_heads"]), int(prob["num_kv_heads"])
+    causal = bool(prob["causal"])
+    scale = float(prob["softmax_scale"])
+    qpos = problem_positions(prob, q_idx)
+    kpos = problem_positions(prob, kv_idx)
+    qr = np.asarray(chunk_buffer_rows(P, len(q_idx), k_q, i))
+    kr = np.asarray(chunk_buffer_rows(P, len(kv_idx), k_kv, j))
+    d = q.shape[2]
+    dq = np.zeros((qr.size, hq, d))
+    dk = np.zeros((kr.size, hkv, d))
+    dv = np.zeros((kr.size, hkv, d))
+    for h in range(hq):
+        hk = q_head_to_kv_head(h, hq, hkv)
+        qh = np.asarray(q[qr, h, :], dtype=np.float64)
+        doh = np.asarray(do[qr, h, :], dtype=np.float64)
+        kh = np.asarray(k[:, hk, :], dtype=np.float64)
+        vh = np.asarray(v[:, hk, :], dtype=np.float64)
+        o, lse = attention_rows(qh, kh, vh, qpos[qr], kpos, causal, scale)
+        D = np.sum(doh * o, axis=1)
+        gq, gk, gv = attention_rows_bwd(qh, kh[kr], vh[kr], doh, lse, D,
+                                        qpos[qr], kpos[kr], causal, scale)
+        dq[:, h] = gq
+        dk[:, hk] += gk
+        dv[:, hk] += gv
+    return dq, dk, dv

@@ -135,3 +135,37 @@ def test_chunk_tasks_accumulate_to_the_tile(layout, kq, kkv):
         np.testing.assert_allclose(o_run, o_tile[qr], rtol=0, atol=1e-12)
         np.testing.assert_allclose(lse_run, lse_tile[:, qr], rtol=0,
                                    atol=1e-12)
+
+
+@pytest.mark.parametrize("kq,kkv", [(2, 3), (3, 1)])
+def test_chunk_backward_sums_to_the_tile(kq, kkv):
+    """dQ of Q chunk i summed over the KV chunks, and dK, dV of KV chunk j
+    summed over the Q chunks, equal the tile's gradients (GQA, causal)."""
+    n, P, d, hq, hkv = 4, 12, 8, 4, 2
+    prob = dict(num_partitions=n, partition_len=P, num_q_heads=hq,
+                num_kv_heads=hkv, head_dim=d, causal=1,
+                softmax_scale=1.0 / math.sqrt(d), layout=1)
+    q_idx, kv_idx = [3, 0], [1, 2, 3]
+    rng = np.random.default_rng(9)
+    q = rng.standard_normal((len(q_idx) * P, hq, d))
+    k = rng.standard_normal((len(kv_idx) * P, hkv, d))
+    v = rng.standard_normal((len(kv_idx) * P, hkv, d))
+    do = rng.standard_normal((len(q_idx) * P, hq, d))
+    tdq, tdk, tdv, heads, _ = oracle.tile_backward(prob, q_idx, kv_idx, q, k,
+                                                   v, do)
+    assert heads == list(range(hq))
+    sdq = np.zeros_like(tdq)
+    sdk = np.zeros_like(tdk)
+    sdv = np.zeros_like(tdv)
+    for i in range(kq):
+        qr = goo.chunk_buffer_rows(P, len(q_idx), kq, i)
+        for j in range(kkv):
+            kr = goo.chunk_buffer_rows(P, len(kv_idx), kkv, j)
+            gq, gk, gv = goo.chunk_backward(prob, q_idx, kv_idx, kq, i, kkv, j,
+                                            q, k, v, do)
+            sdq[qr] += gq
+            sdk[kr] += gk
+            sdv[kr] += gv
+    np.testing.assert_allclose(sdq, tdq, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(sdk, tdk, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(sdv, tdv, rtol=0, atol=1e-12)
