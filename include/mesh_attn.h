@@ -199,6 +199,29 @@ ma_status_t mesh_attn_chunk_fwd(const ma_problem_t* prob, const int32_t* q_idx,
                                 float* lse, int32_t accumulate, void* ws,
                                 size_t ws_bytes, hipStream_t stream);
 
+/* Device workspace bytes mesh_attn_chunk_bwd needs (any chunk of the tile). */
+size_t mesh_attn_chunk_bwd_workspace_size(const ma_problem_t* prob,
+                                          int32_t nq, int32_t nkv);
+
+/* Backward of compute task C-i-j (the per-pair loop of Algorithm 3 over one
+ * chunk pair).  Buffers as in mesh_attn_chunk_fwd: q, o, d_o
+ * [nq*P/k_Q][Hq][d] bf16 (chunk i of every Q partition), lse [Hq][nq*P/k_Q]
+ * (the FINAL LSE of those rows, over the whole key set, with the final O);
+ * k, v [nkv*P/k_KV][Hkv][d] bf16 (chunk j of every KV partition); dq like q,
+ * dk and dv like k, float32.  accumulate 0 overwrites, 1 adds: the tile's dQ
+ * on Q chunk i is the sum of C-i-j over j and its dK, dV on KV chunk j the sum
+ * over i, so a caller zeroes the gradients and accumulates, or orders the
+ * tasks so that each buffer's first task overwrites.  Errors as
+ * mesh_attn_tile_bwd, plus those of the chunk (mesh_attn_chunk_fwd; the
+ * block rows are those of pass 1). */
+ma_status_t mesh_attn_chunk_bwd(const ma_problem_t* prob, const int32_t* q_idx,
+                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                                const ma_chunk_t* chunk, const void* q,
+                                const void* k, const void* v, const void* o,
+                                const void* d_o, const float* lse, float* dq,
+                                float* dk, float* dv, int32_t accumulate,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Kinds of the collective a GOO step runs. */
 enum { MA_GOO_NONE = 0, MA_GOO_AG_Q = 1, MA_GOO_AG_KV = 2, MA_GOO_RS_Q = 3 };
 

@@ -29,6 +29,8 @@ from ._binding import (  # noqa: F401
     mesh_attn_tile_bwd,
     mesh_attn_chunk_fwd_workspace_size,
     mesh_attn_chunk_fwd,
+    mesh_attn_chunk_bwd_workspace_size,
+    mesh_attn_chunk_bwd,
     mesh_attn_goo_plan,
     mesh_attn_last_error,
     Chunk,

@@ -101,6 +101,10 @@ _SIGNATURES = {
     "mesh_attn_chunk_fwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32,
                                    ctypes.POINTER(Chunk), _p, _p, _p, _p, _p,
                                    _i32, _p, _sz, _p]),
+    "mesh_attn_chunk_bwd_workspace_size": (_sz, [_PROB, _i32, _i32]),
+    "mesh_attn_chunk_bwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32,
+                                   ctypes.POINTER(Chunk), _p, _p, _p, _p, _p,
+                                   _p, _p, _p, _p, _i32, _p, _sz, _p]),
     "mesh_attn_goo_plan": (_i32, [_i32, _i32, ctypes.c_double, ctypes.c_double,
                                   ctypes.c_double,
                                   ctypes.POINTER(ctypes.c_double),
@@ -382,6 +386,48 @@ def mesh_attn_chunk_fwd(prob, q_idx, kv_idx, chunk, q, k, v, o, lse,
         _stream_ptr(stream))
     _check("mesh_attn_chunk_fwd", st)
     return o, lse
+
+
+def mesh_attn_chunk_bwd_workspace_size(prob, nq, nkv):
+    return int(load_library().mesh_attn_chunk_bwd_workspace_size(
+        ctypes.byref(Problem.make(prob)), int(nq), int(nkv)))
+
+
+def mesh_attn_chunk_bwd(prob, q_idx, kv_idx, chunk, q, k, v, o, d_o, lse, dq,
+                        dk, dv, accumulate=0, ws=None, stream=None):
+    """Backward of compute task C-i-j, ``chunk = (i, k_q, j, k_kv)``: chunk
+    buffers as in ``mesh_attn_chunk_fwd``, with the final O and LSE of the
+    chunk's Q rows; float32 ``dq`` (Q chunk) and ``dk, dv`` (KV chunk)."""
+    torch = _torch()
+    pr = Problem.make(prob)
+    qa, qp, nq = _idx(q_idx)
+    ka, kp, nkv = _idx(kv_idx)
+    ch = Chunk(*(int(x) for x in chunk))
+    P, hq, hkv, d = (pr.partition_len, pr.num_q_heads, pr.num_kv_heads,
+                     pr.head_dim)
+    if ch.num_q_chunks < 1 or ch.num_kv_chunks < 1:
+        raise ValueError("chunk counts must be >= 1")
+    rq, rk = nq * (P // ch.num_q_chunks), nkv * (P // ch.num_kv_chunks)
+    bf, f32 = (torch.bfloat16,), (torch.float32,)
+    args = [
+        _dev(q, "q", (rq, hq, d), bf),
+        _dev(k, "k", (rk, hkv, d), bf),
+        _dev(v, "v", (rk, hkv, d), bf),
+        _dev(o, "o", (rq, hq, d), bf),
+        _dev(d_o, "d_o", (rq, hq, d), bf),
+        _dev(lse, "lse", (hq, rq), f32),
+        _dev(dq, "dq", (rq, hq, d), f32),
+        _dev(dk, "dk", (rk, hkv, d), f32),
+        _dev(dv, "dv", (rk, hkv, d), f32),
+    ]
+    need = mesh_attn_chunk_bwd_workspace_size(pr, nq, nkv)
+    ws, wsb = _workspace(need, q.device, ws, stream)
+    st = load_library().mesh_attn_chunk_bwd(
+        ctypes.byref(pr), qp, nq, kp, nkv, ctypes.byref(ch), *args,
+        int(accumulate), ctypes.c_void_p(ws.data_ptr()), wsb,
+        _stream_ptr(stream))
+    _check("mesh_attn_chunk_bwd", st)
+    return dq, dk, dv
 
 
 def mesh_attn_goo_plan(k_q, k_kv, t_ag_q, t_ag_kv, t_rs_q, t_c, gamma=1.05):

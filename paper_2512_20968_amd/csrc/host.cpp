@@ -525,6 +525,76 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   return ok();
 }
 
+// Backward of one chunk pair of a tile (the whole tile: one chunk each).
+ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
+                     int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                     const ma_chunk_t& ch, const void* q, const void* k,
+                     const void* v, const void* o, const void* d_o,
+                     const float* lse, float* dq, float* dk, float* dv,
+                     int32_t accumulate, void* ws, size_t ws_bytes,
+                     hipStream_t stream) {
+  ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
+  if (st == MA_OK) st = check_head_dim(prob);
+  if (st == MA_OK) st = check_blocks(prob, kBwdBM, kBwdBN);
+  if (st == MA_OK) st = check_chunk(prob, ch, kBwdBM, kBwdBN);
+  if (st != MA_OK) return st;
+  if (accumulate != 0 && accumulate != 1)
+    return fail(MA_ERR_INVALID_ARG, "accumulate must be 0 or 1, got %d",
+                accumulate);
+  const void* ptrs[] = {q, k, v, o, d_o, lse, dq, dk, dv, ws};
+  const char* names[] = {"q", "k", "v", "o", "d_o", "lse", "dq", "dk", "dv",
+                         "ws"};
+  for (int i = 0; i < 10; ++i) {
+    if (!ptrs[i]) return fail(MA_ERR_INVALID_ARG, "%s is NULL", names[i]);
+    if (!aligned16(ptrs[i]))
+      return fail(MA_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  }
+  const size_t need = bwd_ws_bound(prob, nq, nkv);
+  if (ws_bytes < need)
+    return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
+                ws_bytes, need);
+  std::shared_ptr<Plan> plan;
+  st = get_plan(1, prob, q_idx, nq, kv_idx, nkv, ch, &plan);
+  if (st != MA_OK) return st;
+  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
+                                hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
+  char* wsb = static_cast<char*>(ws);
+  BwdParams bp{};
+  bp.q = static_cast<const uint16_t*>(q);
+  bp.k = static_cast<const uint16_t*>(k);
+  bp.v = static_cast<const uint16_t*>(v);
+  bp.o = static_cast<const uint16_t*>(o);
+  bp.d_o = static_cast<const uint16_t*>(d_o);
+  bp.lse = lse;
+  bp.dq = dq;
+  bp.dk = dk;
+  bp.dv = dv;
+  bp.delta = reinterpret_cast<float*>(wsb + align_up(plan->bytes));
+  bp.lse2 = reinterpret_cast<float*>(
+      wsb + align_up(plan->bytes) +
+      align_up(static_cast<size_t>(nq) * prob->partition_len *
+               prob->num_q_heads * 4));
+  bp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
+  bp.qruns = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
+  bp.qorder = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
+  bp.kvblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->b.off_ptr);
+  bp.kvruns = reinterpret_cast<const DevRun*>(wsb + plan->b.off_runs);
+  bp.kvorder = reinterpret_cast<const int2*>(wsb + plan->b.off_order);
+  bp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
+  bp.rows_kv = int64_t{nkv} * (prob->partition_len / ch.num_kv_chunks);
+  bp.hq = prob->num_q_heads;
+  bp.hkv = prob->num_kv_heads;
+  bp.group = prob->num_q_heads / prob->num_kv_heads;
+  bp.scale = prob->softmax_scale;
+  bp.scale_log2 = prob->softmax_scale * kLog2e;
+  bp.accumulate = accumulate;
+  e = launch_tile_bwd(bp, prob->head_dim, plan->a.grid, plan->b.grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "tile_bwd launch");
+  return ok();
+}
+
+
 }  // namespace
 
 extern "C" {
@@ -689,64 +759,26 @@ ma_status_t mesh_attn_tile_bwd(const ma_problem_t* prob, const int32_t* q_idx,
                                const float* lse, float* dq, float* dk,
                                float* dv, int32_t accumulate, void* ws,
                                size_t ws_bytes, hipStream_t stream) {
-  ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
-  if (st == MA_OK) st = check_head_dim(prob);
-  if (st == MA_OK) st = check_blocks(prob, kBwdBM, kBwdBN);
-  if (st != MA_OK) return st;
-  if (accumulate != 0 && accumulate != 1)
-    return fail(MA_ERR_INVALID_ARG, "accumulate must be 0 or 1, got %d",
-                accumulate);
-  const void* ptrs[] = {q, k, v, o, d_o, lse, dq, dk, dv, ws};
-  const char* names[] = {"q", "k", "v", "o", "d_o", "lse", "dq", "dk", "dv",
-                         "ws"};
-  for (int i = 0; i < 10; ++i) {
-    if (!ptrs[i]) return fail(MA_ERR_INVALID_ARG, "%s is NULL", names[i]);
-    if (!aligned16(ptrs[i]))
-      return fail(MA_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
-  }
-  const size_t need = bwd_ws_bound(prob, nq, nkv);
-  if (ws_bytes < need)
-    return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
-                ws_bytes, need);
-  std::shared_ptr<Plan> plan;
-  st = get_plan(1, prob, q_idx, nq, kv_idx, nkv, kWholeTile, &plan);
-  if (st != MA_OK) return st;
-  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
-                                hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
-  char* wsb = static_cast<char*>(ws);
-  BwdParams bp{};
-  bp.q = static_cast<const uint16_t*>(q);
-  bp.k = static_cast<const uint16_t*>(k);
-  bp.v = static_cast<const uint16_t*>(v);
-  bp.o = static_cast<const uint16_t*>(o);
-  bp.d_o = static_cast<const uint16_t*>(d_o);
-  bp.lse = lse;
-  bp.dq = dq;
-  bp.dk = dk;
-  bp.dv = dv;
-  bp.delta = reinterpret_cast<float*>(wsb + align_up(plan->bytes));
-  bp.lse2 = reinterpret_cast<float*>(
-      wsb + align_up(plan->bytes) +
-      align_up(static_cast<size_t>(nq) * prob->partition_len *
-               prob->num_q_heads * 4));
-  bp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
-  bp.qruns = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
-  bp.qorder = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
-  bp.kvblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->b.off_ptr);
-  bp.kvruns = reinterpret_cast<const DevRun*>(wsb + plan->b.off_runs);
-  bp.kvorder = reinterpret_cast<const int2*>(wsb + plan->b.off_order);
-  bp.rows_q = int64_t{nq} * prob->partition_len;
-  bp.rows_kv = int64_t{nkv} * prob->partition_len;
-  bp.hq = prob->num_q_heads;
-  bp.hkv = prob->num_kv_heads;
-  bp.group = prob->num_q_heads / prob->num_kv_heads;
-  bp.scale = prob->softmax_scale;
-  bp.scale_log2 = prob->softmax_scale * kLog2e;
-  bp.accumulate = accumulate;
-  e = launch_tile_bwd(bp, prob->head_dim, plan->a.grid, plan->b.grid, stream);
-  if (e != hipSuccess) return hip_fail(e, "tile_bwd launch");
-  return ok();
+  return bwd_impl(prob, q_idx, nq, kv_idx, nkv, kWholeTile, q, k, v, o, d_o,
+                  lse, dq, dk, dv, accumulate, ws, ws_bytes, stream);
+}
+
+size_t mesh_attn_chunk_bwd_workspace_size(const ma_problem_t* prob,
+                                          int32_t nq, int32_t nkv) {
+  // A chunk's work lists and row buffers never exceed the whole tile's.
+  return mesh_attn_bwd_workspace_size(prob, nq, nkv);
+}
+
+ma_status_t mesh_attn_chunk_bwd(const ma_problem_t* prob, const int32_t* q_idx,
+                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                                const ma_chunk_t* chunk, const void* q,
+                                const void* k, const void* v, const void* o,
+                                const void* d_o, const float* lse, float* dq,
+                                float* dk, float* dv, int32_t accumulate,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!chunk) return fail(MA_ERR_INVALID_ARG, "chunk is NULL");
+  return bwd_impl(prob, q_idx, nq, kv_idx, nkv, *chunk, q, k, v, o, d_o, lse,
+                  dq, dk, dv, accumulate, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -14,7 +14,7 @@ import paper_2512_20968_amd as ma
 from mesh_inputs import CONFIGS, make_qkv, sample_rows
 from oracle import goo
 
-from helpers import check_fwd, log, run_fwd, to_np
+from helpers import check_fwd, check_grad, log, run_fwd, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -138,3 +138,56 @@ def test_config2_in_4x4_chunk_tasks(gpu):
     rr = torch.tensor(rows, device=gpu)
     check_fwd("config 2 as 4x4 chunks", to_np(o_all[rr][:, heads]),
               to_np(l_all[heads][:, rr]), ro, rl)
+
+
+@pytest.mark.parametrize("layout,kq,kkv", [(0, 2, 2), (1, 1, 4), (1, 4, 1)])
+def test_chunk_backward_sums_to_the_tile(gpu, layout, kq, kkv):
+    """Every C-i-j backward, accumulated into zeroed gradients, against the
+    oracle's tile gradients (every row), and one chunk task alone against the
+    oracle's chunk backward."""
+    from mesh_inputs import make_grad
+    cfg = _small(layout, grad_seed=52)
+    q, k, v, _ = make_qkv(cfg)
+    do = make_grad(cfg)
+    qd, kd, vd, dod = (t.to(gpu) for t in (q, k, v, do))
+    prob = cfg.problem()
+    P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
+                     cfg.head_dim)
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    dq = torch.zeros((cfg.nq * P, hq, d), dtype=torch.float32, device=gpu)
+    dk = torch.zeros((cfg.nkv * P, hkv, d), dtype=torch.float32, device=gpu)
+    dv = torch.zeros_like(dk)
+    single = None
+    for i in range(kq):
+        qr = _rows(P, cfg.nq, kq, i, gpu)
+        qc, oc, doc = (t[qr].contiguous() for t in (qd, o, dod))
+        lc = lse[:, qr].contiguous()
+        for j in range(kkv):
+            kr = _rows(P, cfg.nkv, kkv, j, gpu)
+            kc, vc = kd[kr].contiguous(), vd[kr].contiguous()
+            gq = torch.zeros((qc.shape[0], hq, d), dtype=torch.float32,
+                             device=gpu)
+            gk = torch.zeros((kc.shape[0], hkv, d), dtype=torch.float32,
+                             device=gpu)
+            gv = torch.zeros_like(gk)
+            ma.mesh_attn_chunk_bwd(prob, cfg.q_idx, cfg.kv_idx,
+                                   (i, kq, j, kkv), qc, kc, vc, oc, doc, lc,
+                                   gq, gk, gv, accumulate=1)
+            dq[qr] += gq
+            dk[kr] += gk
+            dv[kr] += gv
+            if single is None:
+                single = (i, j, gq, gk, gv)
+    torch.cuda.synchronize()
+    rdq, rdk, rdv, _, _ = oracle.tile_backward(
+        prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do))
+    tag = f"chunk bwd {kq}x{kkv} layout={layout}"
+    check_grad(f"{tag} dq", to_np(dq), rdq)
+    check_grad(f"{tag} dk", to_np(dk), rdk)
+    check_grad(f"{tag} dv", to_np(dv), rdv)
+    i, j, gq, gk, gv = single
+    cq, ck, cv = goo.chunk_backward(prob, cfg.q_idx, cfg.kv_idx, kq, i, kkv, j,
+                                    to_np(q), to_np(k), to_np(v), to_np(do))
+    check_grad(f"{tag} C-{i}-{j} dq", to_np(gq), cq)
+    check_grad(f"{tag} C-{i}-{j} dk", to_np(gk), ck)
+    check_grad(f"{tag} C-{i}-{j} dv", to_np(gv), cv)
