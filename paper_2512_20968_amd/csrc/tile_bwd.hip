@@ -186,18 +186,24 @@ template <int D>
 struct DkdvLayout {
   static constexpr int TILE = StageTile<D>::BYTES;
   static constexpr int STAGE = 2 * TILE + 2 * SUB * 4;  // Q, dO, lse2, delta
-  static constexpr int SMEM = 2 * STAGE;
+  static constexpr int NSTAGE = 3;
+  // P of one stage, bf16, in the dV waves' register layout: [key wave 4]
+  // [query tile 2][half 2][lane 64] x 16 bytes.
+  static constexpr int PBUF = 4 * 2 * 2 * 64 * 16;
+  static constexpr int SMEM = NSTAGE * STAGE + 2 * PBUF;
 };
 
 constexpr int NT_KV = 512;  // dK/dV: eight waves
 
 // Eight waves in two roles over the same 128 keys (wave w: keys 32*(w%4) ..
-// +32): waves 0-3 accumulate dV (S, P, dV += P^T dO), waves 4-7 dK (S, dP,
-// dS, dK += dS^T Q).  S is computed by both roles (5 products per stage pair
-// instead of 4), but each wave then holds one accumulator and its operand
-// fragments in 256 registers, so two waves share each SIMD and one's MFMAs
-// run while the other works on its softmax; the fused one-wave-per-SIMD form
-// needs dK, dV, K and V fragments together and runs out of registers.
+// +32).  Waves 0-3 (dV role) compute S = Q K^T, P = exp(s S - LSE) and
+// dV += P^T dO for stage t, and leave P (bf16) in LDS; waves 4-7 (dK role)
+// follow one stage behind: dP = dO V^T, dS = P (dP - D) with the P of stage
+// t-1 from LDS, dK += dS^T Q.  Four products per (key block, query stage)
+// as in the algorithm, split evenly between the roles, and each wave needs
+// one accumulator and its operand fragments, so it fits 256 registers and
+// two waves share each SIMD.  Stage tiles are kept three deep (the dK role
+// reads stage t-1 while the dV role reads t and t+1 loads).
 template <int D, int ROLE>
 __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
                                           int kvblk, int hk, int run_b,
@@ -209,9 +215,9 @@ __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
   const int k_in_blk = kw * 32 + li;
   const int64_t kv_row = int64_t{kvblk} * BK + k_in_blk;
 
-  bf16x8 kf[D / 16], vf[D / 16];
-  load_frags<D>(kf, p.k, kv_row, p.hkv, hk, lh);
-  if constexpr (ROLE == 1) load_frags<D>(vf, p.v, kv_row, p.hkv, hk, lh);
+  // dV role: K fragments (B operand of S); dK role: V fragments (of dP).
+  bf16x8 frag[D / 16];
+  load_frags<D>(frag, ROLE == 0 ? p.k : p.v, kv_row, p.hkv, hk, lh);
 
   f32x16 acc[D / 32];
 #pragma unroll
@@ -220,12 +226,15 @@ __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
   if (run_b < run_e) {
     TileAddr<D> ta;
     ta.init(lane, wave, 0);
+    bf16x8* pbuf = reinterpret_cast<bf16x8*>(smem + L::NSTAGE * L::STAGE);
     // Stage cursor over (query head of the group, run, block in run, half).
     struct Cur {
       int g, r, off, s;
       DevRun run;
+      bool valid;
     };
-    auto advance = [&](Cur c, bool* valid) {
+    auto advance = [&](Cur c) {
+      if (!c.valid) return c;
       if (++c.s == 2) {
         c.s = 0;
         if (++c.off == c.run.nblk) {
@@ -237,7 +246,7 @@ __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
           c.run = load_const(p.kvruns, c.r);
         }
       }
-      *valid = c.g < p.group;
+      c.valid = c.g < p.group;
       return c;
     };
     auto issue = [&](const Cur& c, int buf) {
@@ -253,129 +262,149 @@ __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
                                        f + SUB, lane);
     };
 
-    Cur cur{0, run_b, 0, 0, load_const(p.kvruns, run_b)};
-    issue(cur, 0);
+    // Stages: every query head of the group x every block of the runs x 2.
+    int nstage = 0;
+    for (int r = run_b; r < run_e; ++r) nstage += load_const(p.kvruns, r).nblk;
+    nstage *= 2 * p.group;
+    // Iterations t = 0 .. nstage: loads of stage t+1; the dV role computes
+    // stage t (t < nstage), the dK role stage t-1 (t >= 1).  Every iteration
+    // but the last ends with a barrier, the same count in both roles.  Stage
+    // j lives in buffer j % 3 (its previous occupant, stage j-3, was last
+    // read by the dK role in iteration j-2) and its P in P buffer j % 2.
+    Cur lc{0, run_b, 0, 0, load_const(p.kvruns, run_b), true};  // next load
+    Cur cc_ = lc;  // stage this wave computes next
+    issue(lc, 0);
+    lc = advance(lc);
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      wait_for(kf[kk]);
-      if constexpr (ROLE == 1) wait_for(vf[kk]);
-    }
+    for (int kk = 0; kk < D / 16; ++kk) wait_for(frag[kk]);
     wait_vmem();
     __syncthreads();
-    int buf = 0;
-    while (true) {
-      bool has_next;
-      const Cur nxt = advance(cur, &has_next);
-      if (has_next) issue(nxt, buf ^ 1);
-
-      const char* base = smem + buf * L::STAGE;
-      const char* sq = base;
-      const char* sdo = base + L::TILE;
-      const float* slse = reinterpret_cast<const float*>(base + 2 * L::TILE);
-      const float* sdlt = slse + SUB;
-      const int lim = k_in_blk - cur.run.delta - cur.off * BQ - cur.s * SUB;
-
+    int lbuf = 1;   // buffer of the stage loaded next
+    int cbuf = 0;   // buffer of the stage computed next
+    int pb_i = 0;   // P buffer of that stage
+    for (int t = 0; t <= nstage; ++t) {
+      if (t + 1 < nstage) {
+        issue(lc, lbuf);
+        lc = advance(lc);
+        lbuf = lbuf == L::NSTAGE - 1 ? 0 : lbuf + 1;
+      }
+      const bool work = ROLE == 0 ? t < nstage : t >= 1;
+      if (work) {
+        const char* base = smem + cbuf * L::STAGE;
+        const char* sq = base;
+        const char* sdo = base + L::TILE;
+        const float* slse =
+            reinterpret_cast<const float*>(base + 2 * L::TILE);
+        const float* sdlt = slse + SUB;
+        const int lim =
+            k_in_blk - cc_.run.delta - cc_.off * BQ - cc_.s * SUB;
+        bf16x8* pst = pbuf + pb_i * (L::PBUF / 16) + kw * 256;
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        // S = Q K^T (and for dK, dP = dO V^T) of 32 queries; lane li owns
-        // key k_in_blk, register i owns query 32*qt + acc_row(i, lh).
-        __builtin_amdgcn_sched_barrier(0);
-        f32x16 sc, dp;
-        zero(sc);
-        if constexpr (ROLE == 1) zero(dp);
+        for (int qt = 0; qt < 2; ++qt) {
+          __builtin_amdgcn_sched_barrier(0);
+          // dV role: S = Q K^T; dK role: dP = dO V^T.  Lane li owns key
+          // k_in_blk, register i owns query 32*qt + acc_row(i, lh).
+          f32x16 x;
+          zero(x);
+          const char* at = ROLE == 0 ? sq : sdo;
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          sc = mfma32(read_row_op<D>(sq, ta.row, qt, kk), kf[kk], sc);
-          if constexpr (ROLE == 1)
-            dp = mfma32(read_row_op<D>(sdo, ta.row, qt, kk), vf[kk], dp);
-        }
-        {
-          constexpr int NM = (ROLE == 1 ? 2 : 1) * D / 16;
-          __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+          for (int kk = 0; kk < D / 16; ++kk)
+            x = mfma32(read_row_op<D>(at, ta.row, qt, kk), frag[kk], x);
+          {
+            constexpr int NM = D / 16;
+            __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
 #pragma unroll
-          for (int i = 0; i < NM - 3; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            for (int i = 0; i < NM - 3; ++i) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
-        }
-        if (cur.run.cls == 1) {
-          // key k of the block is hidden from query q of the run iff
-          // k - q > delta + (offset of this stage in the run).
+          bf16x8 op[2];  // P (dV role) or dS (dK role), k-contiguous
+          if constexpr (ROLE == 0) {
+            if (cc_.run.cls == 1) {
+              // key k of the block is hidden from query q of the run iff
+              // k - q > delta + (offset of this stage in the run).
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            if (qt * 32 + acc_row(i, lh) < lim) sc[i] = -INFINITY;
-        }
-        bf16x8 op[2];  // P (dV) or dS (dK), k-contiguous per lane half
+              for (int i = 0; i < 16; ++i)
+                if (qt * 32 + acc_row(i, lh) < lim) x[i] = -INFINITY;
+            }
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int q0 = qt * 32 + hh * 16 + lh * 8;
-          const f32x4 l0 = *reinterpret_cast<const f32x4*>(slse + q0);
-          const f32x4 l1 = *reinterpret_cast<const f32x4*>(slse + q0 + 4);
-          f32x4 d0, d1;
-          if constexpr (ROLE == 1) {
-            d0 = *reinterpret_cast<const f32x4*>(sdlt + q0);
-            d1 = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4);
-          }
+            for (int hh = 0; hh < 2; ++hh) {
+              const int q0 = qt * 32 + hh * 16 + lh * 8;
+              const f32x4 l0 = *reinterpret_cast<const f32x4*>(slse + q0);
+              const f32x4 l1 = *reinterpret_cast<const f32x4*>(slse + q0 + 4);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int i = hh * 8 + e;
-            const float lq = e < 4 ? l0[e] : l1[e - 4];
-            const float pv = exp2_fast(fmaf(sc[i], p.scale_log2, -lq));
-            if constexpr (ROLE == 0) {
-              op[hh][e] = static_cast<__bf16>(pv);
-            } else {
-              const float dq = e < 4 ? d0[e] : d1[e - 4];
-              op[hh][e] = static_cast<__bf16>(pv * (dp[i] - dq));
+              for (int e = 0; e < 8; ++e) {
+                const float lq = e < 4 ? l0[e] : l1[e - 4];
+                op[hh][e] = static_cast<__bf16>(
+                    exp2_fast(fmaf(x[hh * 8 + e], p.scale_log2, -lq)));
+              }
+              pst[(qt * 2 + hh) * 64 + lane] = op[hh];
+            }
+          } else {
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+              const int q0 = qt * 32 + hh * 16 + lh * 8;
+              const f32x4 d0 = *reinterpret_cast<const f32x4*>(sdlt + q0);
+              const f32x4 d1 = *reinterpret_cast<const f32x4*>(sdlt + q0 + 4);
+              const bf16x8 pv = pst[(qt * 2 + hh) * 64 + lane];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float dq = e < 4 ? d0[e] : d1[e - 4];
+                op[hh][e] = static_cast<__bf16>(static_cast<float>(pv[e]) *
+                                                (x[hh * 8 + e] - dq));
+              }
             }
           }
-        }
-        // dV += P^T dO or dK += dS^T Q (scale at the end); the B operand is
-        // read transposed from the dO or Q row tile.  A scheduling region of
-        // its own, so that the read-ahead pattern below is not mixed with the
-        // VALU work above.
-        __builtin_amdgcn_sched_barrier(0);
-        const char* bt = ROLE == 0 ? sdo : sq;
+          // dV += P^T dO or dK += dS^T Q (scale at the end); the B operand
+          // is read transposed from the dO or Q row tile.
+          __builtin_amdgcn_sched_barrier(0);
+          const char* bt = ROLE == 0 ? sdo : sq;
 #pragma unroll
-        for (int cc = 0; cc < D / 32; ++cc)
+          for (int c = 0; c < D / 32; ++c)
 #pragma unroll
-          for (int hh = 0; hh < 2; ++hh)
-            acc[cc] = mfma32(op[hh], read_tr_op<D>(bt, ta, cc, 2 * qt + hh),
-                             acc[cc]);
-        {
-          constexpr int NM = D / 16;  // two transpose reads per MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+            for (int hh = 0; hh < 2; ++hh)
+              acc[c] = mfma32(op[hh], read_tr_op<D>(bt, ta, c, 2 * qt + hh),
+                              acc[c]);
+          {
+            constexpr int NM = D / 16;  // two transpose reads per MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-          for (int i = 0; i < NM - 3; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            for (int i = 0; i < NM - 3; ++i) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
         }
       }
-
-      if (!has_next) break;
-      wait_vmem();
-      lds_barrier();  // stage buf^1 landed; every wave is done with buf
-      buf ^= 1;
-      cur = nxt;
+      if (work) {
+        cc_ = advance(cc_);
+        cbuf = cbuf == L::NSTAGE - 1 ? 0 : cbuf + 1;
+        pb_i ^= 1;
+      }
+      if (t < nstage) {
+        wait_vmem();
+        lds_barrier();
+      }
     }
   }
 
-  // Accumulator register i of chunk cc: key row 8*(i/4) + 4*lh + i%4 of the
-  // wave's 32 keys, dim 32*cc + li.
+  // Accumulator register i of chunk c: key row 8*(i/4) + 4*lh + i%4 of the
+  // wave's 32 keys, dim 32*c + li.
   float* out = ROLE == 0 ? p.dv : p.dk;
   const float sc_out = ROLE == 0 ? 1.f : p.scale;
 #pragma unroll
-  for (int cc = 0; cc < D / 32; ++cc)
+  for (int c = 0; c < D / 32; ++c)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int64_t row =
           int64_t{kvblk} * BK + kw * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
-      const int64_t idx = (row * p.hkv + hk) * D + cc * 32 + li;
-      float x = acc[cc][i] * sc_out;
-      if (p.accumulate) x += out[idx];
-      out[idx] = x;
+      const int64_t idx = (row * p.hkv + hk) * D + c * 32 + li;
+      float v = acc[c][i] * sc_out;
+      if (p.accumulate) v += out[idx];
+      out[idx] = v;
     }
 }
 
