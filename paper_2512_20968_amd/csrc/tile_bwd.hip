@@ -393,19 +393,29 @@ __device__ __forceinline__ void dkdv_role(const BwdParams& p, char* smem,
 
   // Accumulator register i of chunk c: key row 8*(i/4) + 4*lh + i%4 of the
   // wave's 32 keys, dim 32*c + li.
+  // With accumulate, every old value is read before the first store, so the
+  // loads are issued back to back instead of one read-modify-write at a time.
   float* out = ROLE == 0 ? p.dv : p.dk;
   const float sc_out = ROLE == 0 ? 1.f : p.scale;
+  auto index = [&](int c, int i) {
+    const int64_t row =
+        int64_t{kvblk} * BK + kw * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
+    return (row * p.hkv + hk) * D + c * 32 + li;
+  };
+  f32x16 prev[D / 32];
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) zero(prev[c]);
+  if (p.accumulate) {
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) prev[c][i] = out[index(c, i)];
+  }
 #pragma unroll
   for (int c = 0; c < D / 32; ++c)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int64_t row =
-          int64_t{kvblk} * BK + kw * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
-      const int64_t idx = (row * p.hkv + hk) * D + c * 32 + li;
-      float v = acc[c][i] * sc_out;
-      if (p.accumulate) v += out[idx];
-      out[idx] = v;
-    }
+    for (int i = 0; i < 16; ++i)
+      out[index(c, i)] = fmaf(acc[c][i], sc_out, prev[c][i]);
 }
 
 template <int D>
@@ -580,18 +590,30 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
   }
 
   // Register 4g+t of chunk cc holds dim 32cc + 8g + 4lh + t of query q_row.
+  // With accumulate, all old values are read before the first store.
   float* dst = p.dq + (q_row * p.hq + h) * D;
+  f32x4 prev[D / 32][4];
+#pragma unroll
+  for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) prev[cc][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (p.accumulate) {
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        prev[cc][g] = *reinterpret_cast<const f32x4*>(
+            dst + cc * 32 + g * 8 + lh * 4);
+  }
 #pragma unroll
   for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int dim = cc * 32 + g * 8 + lh * 4;
       f32x4 val;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) val[t] = acc[cc][4 * g + t] * p.scale;
-      f32x4* out = reinterpret_cast<f32x4*>(dst + dim);
-      if (p.accumulate) val += *out;
-      *out = val;
+      for (int t = 0; t < 4; ++t)
+        val[t] = fmaf(acc[cc][4 * g + t], p.scale, prev[cc][g][t]);
+      *reinterpret_cast<f32x4*>(dst + cc * 32 + g * 8 + lh * 4) = val;
     }
 }
 

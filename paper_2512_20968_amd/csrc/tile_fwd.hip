@@ -459,6 +459,24 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
   // O^T accumulator: register 4g+t of chunk cc holds dim 32cc + 8g + 4lh + t.
   const int64_t obase = (q_row * p.hq + h) * D;
   const float sc_new = inv * w_new;
+  // Accumulating: every stored value is read before the first store, so the
+  // loads are issued back to back.
+  f32x4 prev[OUT_F32 ? D / 32 : 1][4];
+  if constexpr (OUT_F32) {
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) prev[cc][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (p.accumulate) {
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          prev[cc][g] = *reinterpret_cast<const f32x4*>(
+              static_cast<const float*>(p.o) + obase + cc * 32 + g * 8 +
+              lh * 4);
+    }
+  }
 #pragma unroll
   for (int cc = 0; cc < D / 32; ++cc)
 #pragma unroll
@@ -470,11 +488,8 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
       if constexpr (OUT_F32) {
         f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(p.o) + obase +
                                               dim);
-        if (p.accumulate) {
-          const f32x4 prev = *dst;
 #pragma unroll
-          for (int t = 0; t < 4; ++t) x[t] = fmaf(w_old, prev[t], x[t]);
-        }
+        for (int t = 0; t < 4; ++t) x[t] = fmaf(w_old, prev[cc][g][t], x[t]);
         *dst = x;
       } else {
         bf16x4 val;
