@@ -168,6 +168,10 @@ def test_forward_is_deterministic(gpu):
     (5, 777, 2, 128, torch.bfloat16, torch.bfloat16, 0.3),
     (16, 4096, 4, 128, torch.bfloat16, torch.float32, 0.0),
     (9, 333, 1, 8, torch.float32, torch.float32, 0.5),
+    # more partials than one load batch (16 bf16 / 8 float32 per batch): the
+    # running reducer across batches and a ragged last batch
+    (17, 200, 2, 128, torch.bfloat16, torch.bfloat16, 0.2),
+    (33, 100, 2, 64, torch.float32, torch.float32, 0.3),
 ])
 def test_merge_parity(gpu, kparts, rows, heads, d, in_dt, out_dt, ninf):
     o, lse = make_merge_parts(kparts, rows, heads, d, seed=kparts + rows,
