@@ -22,8 +22,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;  // four waves
 constexpr int kTileRows = 64;  // rows of a staged tile
@@ -100,91 +98,6 @@ __device__ __forceinline__ int acc_row(int r, int h) {
   return (r >> 3) * 16 + h * 8 + (r & 7);
 }
 
-template <int D>
-__device__ __forceinline__ int row_chunk(int row, int chunk) {
-  return chunk ^ (D == 128 ? (row & 15) : (row & 7));
-}
-__device__ __forceinline__ int col_chunk(int dim, int chunk) {
-  return chunk ^ ((dim ^ (dim >> 3)) & 7);
-}
-
-// 16-byte A/B operand read from a row-major [64][D] tile: row `row`, dims
-// 16*kk + 8*h .. +7.
-template <int D>
-__device__ __forceinline__ bf16x8 read_rows(const uint16_t* t, int row, int kk,
-                                            int h) {
-  return *reinterpret_cast<const bf16x8*>(
-      t + row * D + row_chunk<D>(row, 2 * kk + h) * 8);
-}
-
-// 16-byte operand read from a transposed [D][64] tile: dim `dim`, rows
-// 16*ss + 8*h .. +7.
-__device__ __forceinline__ bf16x8 read_cols(const uint16_t* t, int dim, int ss,
-                                            int h) {
-  return *reinterpret_cast<const bf16x8*>(
-      t + dim * kTileRows + col_chunk(dim, 2 * ss + h) * 8);
-}
-
-__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
-  return (a & 0xffffu) | (b << 16);
-}
-__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
-  return (a >> 16) | (b & 0xffff0000u);
-}
-
-// 64 rows x D of one head, global -> registers -> LDS.  Thread t owns the
-// 16-byte chunk t % (D/8) of NLD consecutive rows, so a wave's loads cover
-// whole 2*D-byte row segments (coalesced) and the transposed store needs only
-// an in-register NLD x 8 transpose.
-template <int D>
-struct RowTile {
-  static constexpr int CPR = D / 8;
-  static constexpr int NLD = kTileRows * CPR / kThreads;  // 4 (D=128), 2 (64)
-  static_assert(NLD == 2 || NLD == 4, "unsupported head_dim");
-  u32x4 r[NLD];
-
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ g,
-                                       int64_t row0, int heads, int head,
-                                       int tid) {
-    const int c = tid % CPR;
-    const int64_t rb = row0 + (tid / CPR) * NLD;
-#pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      r[j] = *reinterpret_cast<const u32x4*>(
-          g + ((rb + j) * heads + head) * D + c * 8);
-  }
-
-  __device__ __forceinline__ void store_rows(uint16_t* t, int tid) const {
-    const int c = tid % CPR;
-    const int rb = (tid / CPR) * NLD;
-#pragma unroll
-    for (int j = 0; j < NLD; ++j)
-      *reinterpret_cast<u32x4*>(t + (rb + j) * D + row_chunk<D>(rb + j, c) * 8) =
-          r[j];
-  }
-
-  __device__ __forceinline__ void store_cols(uint16_t* t, int tid) const {
-    const int c = tid % CPR;
-    const int rb = (tid / CPR) * NLD;
-    const int chunk = rb >> 3, sub = rb & 7;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int dim = c * 8 + e;
-      const int w = e >> 1;
-      uint16_t* p = t + dim * kTileRows + col_chunk(dim, chunk) * 8 + sub;
-      if constexpr (NLD == 4) {
-        u32x2 val;
-        val[0] = (e & 1) ? pack_hi(r[0][w], r[1][w]) : pack_lo(r[0][w], r[1][w]);
-        val[1] = (e & 1) ? pack_hi(r[2][w], r[3][w]) : pack_lo(r[2][w], r[3][w]);
-        *reinterpret_cast<u32x2*>(p) = val;
-      } else {
-        *reinterpret_cast<uint32_t*>(p) =
-            (e & 1) ? pack_hi(r[0][w], r[1][w]) : pack_lo(r[0][w], r[1][w]);
-      }
-    }
-  }
-};
-
 // Operand fragments of 32 rows held in registers for a whole workgroup
 // item: lane (l % 32, half h) holds row l % 32, dims 16*kk + 8*h .. +7.
 template <int D>
@@ -210,12 +123,6 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   // Word 3 = 0x00020000: 32-bit data format, the gfx9-family setting.
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
                                            static_cast<int>(bytes), 0x00020000);
-}
-
-__device__ __forceinline__ u32x4 buffer_load16(rsrc_t r, uint32_t voff,
-                                               uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(voff),
-                                               static_cast<int>(soff), 0);
 }
 
 // Direct global -> LDS load of 16 bytes per lane (buffer_load_dwordx4 ... lds):
