@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace mesh_attn {
 
 // gfx950 (MI355X) has 8 XCDs; consecutive workgroup ids are dispatched to
@@ -87,5 +89,26 @@ struct BwdParams {
 
 hipError_t launch_tile_bwd(const BwdParams& p, int head_dim, int grid_q,
                            int grid_kv, hipStream_t stream);
+
+// Kernels with more than 64 KB of dynamic LDS need the limit raised once per
+// kernel and device; this does it on the first launch on each device (ids
+// below 64; higher ids set it on every launch).  Safe to call from several
+// threads: the attribute set is idempotent and the flags are atomic.
+template <auto Kern>
+hipError_t ensure_dynamic_lds(size_t bytes) {
+  static std::atomic<uint64_t> done{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev >= 0 && dev < 64 ? uint64_t{1} << dev : 0;
+  if (bit != 0 && (done.load(std::memory_order_acquire) & bit) != 0)
+    return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(Kern),
+                          hipFuncAttributeMaxDynamicSharedMemorySize,
+                          static_cast<int>(bytes));
+  if (e == hipSuccess && bit != 0)
+    done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
 
 }  // namespace mesh_attn

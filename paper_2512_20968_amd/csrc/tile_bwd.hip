@@ -617,24 +617,15 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
     }
 }
 
-template <typename K>
-hipError_t set_smem(K kern, size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                             static_cast<int>(bytes));
-}
-
 template <int D>
 hipError_t launch(const BwdParams& p, int grid_q, int grid_kv,
                   hipStream_t stream) {
   const size_t smem_kv = DkdvLayout<D>::SMEM;
   const size_t smem_q = DqLayout<D>::SMEM;
-  static bool attr_done = false;  // benign race: idempotent attribute set
-  if (!attr_done) {
-    hipError_t e = set_smem(bwd_dkdv_kernel<D>, smem_kv);
-    if (e == hipSuccess) e = set_smem(bwd_dq_kernel<D>, smem_q);
+  {
+    hipError_t e = ensure_dynamic_lds<bwd_dkdv_kernel<D>>(smem_kv);
+    if (e == hipSuccess) e = ensure_dynamic_lds<bwd_dq_kernel<D>>(smem_q);
     if (e != hipSuccess) return e;
-    attr_done = true;
   }
   const int64_t prep_threads = p.rows_q * p.hq * (D / 8);
   const int prep_grid = static_cast<int>((prep_threads + NT - 1) / NT);

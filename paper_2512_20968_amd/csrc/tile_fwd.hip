@@ -504,16 +504,10 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
 template <int D, bool F32>
 hipError_t launch(const FwdParams& p, int grid, hipStream_t stream) {
   const size_t smem = FwdLayout<D>::SMEM;
-  auto kern = tile_fwd_kernel<D, F32>;
-  static bool attr_done = false;  // benign race: idempotent attribute set
-  if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(kern),
-        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
-    if (e != hipSuccess) return e;
-    attr_done = true;
-  }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NT), smem, stream, p);
+  const hipError_t e = ensure_dynamic_lds<tile_fwd_kernel<D, F32>>(smem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((tile_fwd_kernel<D, F32>), dim3(grid), dim3(NT), smem,
+                     stream, p);
   return hipGetLastError();
 }
 
