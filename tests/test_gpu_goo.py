@@ -191,3 +191,55 @@ def test_chunk_backward_sums_to_the_tile(gpu, layout, kq, kkv):
     check_grad(f"{tag} C-{i}-{j} dq", to_np(gq), cq)
     check_grad(f"{tag} C-{i}-{j} dk", to_np(gk), ck)
     check_grad(f"{tag} C-{i}-{j} dv", to_np(gv), cv)
+
+
+def test_config5_backward_as_2x2_chunk_tasks(gpu):
+    """The full-size causal 64K backward as 2 x 2 chunk tasks accumulated into
+    zeroed gradients: every row against the fused tile backward (itself
+    checked against the oracle in test_gpu_bwd), within the summation-order
+    tolerance of the gradients."""
+    from mesh_inputs import make_grad
+    cfg = CONFIGS[5]
+    q, k, v, _ = make_qkv(cfg)
+    do = make_grad(cfg)
+    qd, kd, vd, dod = (t.to(gpu) for t in (q, k, v, do))
+    prob = cfg.problem()
+    P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
+                     cfg.head_dim)
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    fdq = torch.empty((cfg.nq * P, hq, d), dtype=torch.float32, device=gpu)
+    fdk = torch.empty((cfg.nkv * P, hkv, d), dtype=torch.float32, device=gpu)
+    fdv = torch.empty_like(fdk)
+    ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o, dod,
+                          lse, fdq, fdk, fdv)
+    kq = kkv = 2
+    dq = torch.zeros_like(fdq)
+    dk = torch.zeros_like(fdk)
+    dv = torch.zeros_like(fdk)
+    log("config 5: backward as 2x2 chunk tasks")
+    for i in range(kq):
+        qr = _rows(P, cfg.nq, kq, i, gpu)
+        qc, oc, doc = (t[qr].contiguous() for t in (qd, o, dod))
+        lc = lse[:, qr].contiguous()
+        gq = torch.zeros((qc.shape[0], hq, d), dtype=torch.float32,
+                         device=gpu)
+        for j in range(kkv):
+            kr = _rows(P, cfg.nkv, kkv, j, gpu)
+            kc, vc = kd[kr].contiguous(), vd[kr].contiguous()
+            gk = dk[kr].contiguous()
+            gv = dv[kr].contiguous()
+            # accumulate: dQ over the KV chunks, dK/dV over the Q chunks
+            ma.mesh_attn_chunk_bwd(prob, cfg.q_idx, cfg.kv_idx,
+                                   (i, kq, j, kkv), qc, kc, vc, oc, doc, lc,
+                                   gq, gk, gv, accumulate=1)
+            dk[kr] = gk
+            dv[kr] = gv
+        dq[qr] = gq
+    torch.cuda.synchronize()
+    for name, got, ref in (("dq", dq, fdq), ("dk", dk, fdk), ("dv", dv, fdv)):
+        err = float((got - ref).abs().max())
+        scale = float(ref.abs().max())
+        log(f"config 5 chunks vs fused {name}: max err {err:.3e}, "
+            f"max |{name}| {scale:.3e}")
+        # same products, different fp32 summation order across the chunks
+        assert err <= 1e-3 * scale, name
