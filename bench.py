@@ -9,14 +9,17 @@ resident in HBM:
          head_dim 128, bf16): work list, scores, causal mask, online softmax,
          PV, epilogue.
   merge  mesh_attn_lse_merge folding 16 bf16 partials of 4096 rows x 32
-         heads x 128 (the reduce-scatter fold of a 16x16 mesh).
+         heads x 128 (the reduce-scatter fold of a 16x16 mesh); two copies of
+         the partials alternate between steps, so the reads come from HBM.
   bwd    mesh_attn_tile_bwd of the same causal tile (dO from seed 4), using
          the forward's O and LSE.
 
 `value` is the forward tile TFLOP/s: algorithmic FLOPs of the tile
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
 duration over the timed steps, measured with HIP events on the launch stream.
-`ms_per_step` is the whole step.  Per-stage figures are under `legs`.
+`ms_per_step` is the whole step.  Per-stage figures are under `legs` (the
+forward's also gives the host time of building the tile's work list, which
+the library caches and which is outside the timed steps).
 Prints one JSON line on stdout; progress goes to stderr.
 """
 
@@ -116,8 +119,20 @@ def cpu_baseline(cfg, budget_s):
             used = max(int(i["num_threads"]) for i in infos)
     dt = time.perf_counter() - t0
     flops = 4.0 * cfg.head_dim * done_heads * float(vis.sum())
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": used,
-            "kind": "oracle",
+    rate = flops / dt
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    cpu_model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    full = 4.0 * cfg.head_dim * cfg.num_q_heads * visible_pairs(cfg)
+    return {"value": rate / 1e12, "unit": "TFLOP/s", "cores": used,
+            "kind": "oracle", "cpu_model": cpu_model,
+            "projected_full_tile_s": round(full / rate, 1),
             "sample": (f"float64 oracle forward of {len(rows)} sampled query "
                        f"rows x {done_heads} heads of the {cfg.name} tile "
                        f"({flops / 1e9:.1f} GFLOP algorithmic, {dt:.1f} s)")}
@@ -207,10 +222,15 @@ def main():
         mk, mrows, mh, md = 16, 4096, 32, 128
         mo_parts, ml_parts = make_merge_parts(mk, mrows, mh, md, seed=7)
         mo_parts, ml_parts = mo_parts.to(dev), ml_parts.to(dev)
+        # Two copies of the partials, used in turn: 545 MB each, more than
+        # the 256 MB last-level cache, so every merge reads from HBM even when
+        # it runs alone (--legs merge).
+        msets = [(mo_parts, ml_parts), (mo_parts.clone(), ml_parts.clone())]
         mo = torch.empty((mrows, mh, md), dtype=torch.bfloat16, device=dev)
         ml = torch.empty((mh, mrows), dtype=torch.float32, device=dev)
 
     stream = torch.cuda.current_stream()
+    step_no = [0]
 
     def run_step(ev=None):
         if "fwd" in legs:
@@ -229,13 +249,14 @@ def main():
             if ev: ev["chunks"][1].record(stream)
         if "merge" in legs:
             if ev: ev["merge"][0].record(stream)
-            ma.mesh_attn_lse_merge(mo_parts, ml_parts, mo, ml)
+            ma.mesh_attn_lse_merge(*msets[step_no[0] % 2], mo, ml)
             if ev: ev["merge"][1].record(stream)
         if "bwd" in legs:
             if ev: ev["bwd"][0].record(stream)
             ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o,
                                   do, lse, dq, dk, dv, ws=ws_b)
             if ev: ev["bwd"][1].record(stream)
+        step_no[0] += 1
 
     if args.calib_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -267,6 +288,13 @@ def main():
     log(f"step {ms_step:.3f} ms; " +
         ", ".join(f"{n} {leg_ms[n]:.3f} ms" for n in legs))
 
+    # Host time of the canonical work list (built once per tile and cached by
+    # the library, so it is outside the timed steps).
+    bm, bn = ma.mesh_attn_block_shape(d, 0)
+    t_wl = time.perf_counter()
+    _, wl_runs = ma.mesh_attn_worklist(prob, cfg.q_idx, cfg.kv_idx, bm, bn)
+    wl_ms = (time.perf_counter() - t_wl) * 1e3
+
     pairs = visible_pairs(cfg)
     fwd_flop = 4.0 * d * hq * pairs
     bwd_flop = 10.0 * d * hq * pairs
@@ -286,7 +314,9 @@ def main():
         out_legs["fwd"] = {"ms": round(leg_ms["fwd"], 4),
                            "tflops": round(tf, 2),
                            "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
-                           "flop": fwd_flop}
+                           "flop": fwd_flop,
+                           "worklist_host_ms": round(wl_ms, 3),
+                           "worklist_runs": int(len(wl_runs))}
     if "chunks" in legs:
         tc = fwd_flop / (leg_ms["chunks"] * 1e-3) / 1e12
         out_legs["chunks"] = {"ms": round(leg_ms["chunks"], 4),
