@@ -6,18 +6,22 @@
 //  1. prep:   D_i = <dO_i, O_i> and LSE_i * log2(e) for every (row, query
 //     head), float32 (a row without a visible key gets +inf, so that its
 //     probabilities exp2(s S - LSE) are 0).
-//  2. dK/dV:  one workgroup per (KV block of 128 keys, KV head), 4 waves x 32
-//     keys.  It walks the KV block's runs of Q blocks (KV-major work list) for
-//     every query head of the GQA group, in 64-row stages, and keeps dK, dV
-//     in registers:  S = Q K^T,  P = exp(s S - LSE),  dP = dO V^T,
-//     dS = P (dP - D),  dV += P^T dO,  dK += s dS^T Q.
+//  2. dK/dV:  one workgroup per (KV block of 128 keys, KV head), eight waves
+//     in two roles over four 32-key groups.  It walks the KV block's runs of
+//     Q blocks (KV-major work list) for every query head of the GQA group, in
+//     64-row stages, and keeps dK, dV in registers.  The dV role computes
+//     S = Q K^T,  P = exp(s S - LSE),  dV += P^T dO  and leaves P in LDS; the
+//     dK role, one stage behind, computes  dP = dO V^T,  dS = P (dP - D),
+//     dK += s dS^T Q.
 //  3. dQ:     one workgroup per (Q block of 128 rows, query head), 4 waves x
-//     32 rows, walking the Q-major runs of KV blocks in 64-key stages:
+//     32 rows (two workgroups per CU), walking the Q-major runs of KV blocks
+//     in 64-key stages:
 //     S^T = K Q^T,  dP^T = V dO^T,  dS^T = P^T (dP^T - D),  dQ^T += s K^T dS^T.
 //
 // The stage tiles (Q and dO, or K and V: 64 rows x d) stream from HBM
-// straight into LDS (buffer loads with the LDS-destination form), double
-// buffered, one barrier per stage.  Each tile is stored once, row-major, and
+// straight into LDS (buffer loads with the LDS-destination form), one barrier
+// per stage; dQ keeps two stages, dK/dV three (the dK role reads the stage
+// before the one the dV role reads).  Each tile is stored once, row-major, and
 // read two ways: as rows (the A operand of the score MFMAs, 16-byte reads) and
 // transposed (the B operand of dV / dK, the A operand of dQ) through the
 // gfx950 LDS transpose read ds_read_b64_tr_b16.  One XOR swizzle of the
