@@ -71,6 +71,33 @@ def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
     check_grad(f"{tag} dv", to_np(dv), rdv)
 
 
+def test_rows_and_keys_nobody_sees(gpu):
+    """Causal tile {0, 2} x {1, 3}: the rows of Q partition 0 see no key and
+    the keys of KV partition 3 are seen by no row.  Their gradient rows must
+    be exactly zero (written into uninitialised outputs), every other row
+    within tolerance of the oracle."""
+    cfg = dataclasses.replace(CONFIGS[1], num_partitions=4, partition_len=256,
+                              q_idx=[0, 2], kv_idx=[1, 3], num_q_heads=4,
+                              num_kv_heads=2, head_dim=128, causal=True,
+                              seed=21, grad_seed=22)
+    P = cfg.partition_len
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    assert torch.all(torch.isneginf(lse[:, :P]))
+    dq, dk, dv = (torch.full_like(t, float("nan"))
+                  for t in _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse))
+    ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o, dod,
+                          lse, dq, dk, dv)
+    torch.cuda.synchronize()
+    assert torch.all(dq[:P] == 0), "dQ of rows without a visible key"
+    assert torch.all(dk[P:] == 0) and torch.all(dv[P:] == 0), \
+        "dK, dV of keys no row sees"
+    rdq, rdk, rdv, _, _ = oracle.tile_backward(
+        prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do))
+    check_grad("unseen rows/keys dq", to_np(dq), rdq)
+    check_grad("unseen rows/keys dk", to_np(dk), rdk)
+    check_grad("unseen rows/keys dv", to_np(dv), rdv)
+
+
 def test_accumulate_adds_into_outputs(gpu):
     cfg = dataclasses.replace(CONFIGS[1], causal=True, seed=31, grad_seed=32)
     prob, _, (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
