@@ -51,6 +51,14 @@ SMALL = [
     ([1, 2], [0, 3], 2, 1, 128, False),
 ]
 
+# Several blocks per partition (P = 1024: 8 dQ Q blocks and 8 dK/dV KV
+# blocks per partition) at both head dims.
+MULTI = [
+    # (q_idx, kv_idx, hq, hkv, d)
+    ([2, 1], [0, 2, 1], 4, 2, 64),
+    ([2, 1], [0, 2, 1], 2, 1, 128),
+]
+
 
 @pytest.mark.parametrize("q_idx,kv_idx,hq,hkv,d,causal", SMALL)
 def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
@@ -66,6 +74,25 @@ def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
     rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
         prob, q_idx, kv_idx, to_np(q), to_np(k), to_np(v), to_np(do))
     tag = f"tile {q_idx}x{kv_idx} hq={hq} hkv={hkv} d={d} c={causal}"
+    check_grad(f"{tag} dq", to_np(dq), rdq)
+    check_grad(f"{tag} dk", to_np(dk), rdk)
+    check_grad(f"{tag} dv", to_np(dv), rdv)
+
+
+@pytest.mark.parametrize("q_idx,kv_idx,hq,hkv,d", MULTI)
+def test_multi_block_partitions_every_row(gpu, q_idx, kv_idx, hq, hkv, d):
+    """Causal GQA tile with 1024-token partitions (diagonal pairs spanning
+    several blocks, a permuted KV list): every row of dQ, dK, dV."""
+    cfg = dataclasses.replace(CONFIGS[1], num_partitions=3,
+                              partition_len=1024, q_idx=q_idx, kv_idx=kv_idx,
+                              num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                              causal=True, seed=41, grad_seed=42)
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    torch.cuda.synchronize()
+    rdq, rdk, rdv, _, _ = oracle.tile_backward(
+        prob, q_idx, kv_idx, to_np(q), to_np(k), to_np(v), to_np(do))
+    tag = f"P=1024 tile {q_idx}x{kv_idx} hq={hq} hkv={hkv} d={d}"
     check_grad(f"{tag} dq", to_np(dq), rdq)
     check_grad(f"{tag} dk", to_np(dk), rdk)
     check_grad(f"{tag} dv", to_np(dv), rdv)

@@ -162,6 +162,26 @@ def test_forward_is_deterministic(gpu):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("d,hq,hkv", [(64, 8, 2), (128, 4, 1)])
+def test_multi_block_partitions_every_row(gpu, d, hq, hkv):
+    """1024-token partitions (four 256-row Q blocks and sixteen 64-key blocks
+    per partition, so diagonal pairs mix FULL, PARTIAL and EMPTY blocks),
+    causal GQA, permuted lists, both head dims: every row checked."""
+    cfg = dataclasses.replace(CONFIGS[1], num_partitions=3,
+                              partition_len=1024, q_idx=[2, 1],
+                              kv_idx=[0, 2, 1], num_q_heads=hq,
+                              num_kv_heads=hkv, head_dim=d, causal=True,
+                              seed=43)
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    prob = cfg.problem()
+    o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
+    torch.cuda.synchronize()
+    ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, to_np(q),
+                                 to_np(k), to_np(v))
+    check_fwd(f"P=1024 causal GQA d={d} hq={hq} hkv={hkv}", to_np(o),
+              to_np(lse), ro, rl)
+
+
 @pytest.mark.parametrize("kparts,rows,heads,d,in_dt,out_dt,ninf", [
     (1, 37, 3, 64, torch.float32, torch.float32, 0.0),
     (2, 1000, 4, 64, torch.float32, torch.bfloat16, 0.1),
