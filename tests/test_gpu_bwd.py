@@ -185,3 +185,43 @@ def test_config5_backward_causal_64k(gpu):
     check_grad("config 5 dq", to_np(dq[qr][:, q_heads]), rdq)
     check_grad("config 5 dk", to_np(dk[kr][:, heads]), rdk)
     check_grad("config 5 dv", to_np(dv[kr][:, heads]), rdv)
+
+
+def test_config3_shape_gqa_backward(gpu):
+    """Backward at the 1M-token non-causal GQA tile's full size (65536 rows,
+    32 query heads on 8 KV heads).  dQ of sampled rows of two query heads (in
+    different KV groups) against the float64 definition on those rows; on
+    every KV head, the identities that hold because each row's softmax runs
+    over exactly the tile's keys: sum_j dK_j = 0 and sum_j dV_j = sum of dO
+    over the rows and the query heads of the group."""
+    from oracle.attention import (attention_rows, attention_rows_bwd,
+                                  problem_positions)
+    cfg = dataclasses.replace(CONFIGS[3], grad_seed=8)
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    log("config 3 shape: GPU backward")
+    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
+    torch.cuda.synchronize()
+    g = cfg.num_q_heads // cfg.num_kv_heads
+    sdk = dk.sum(0)
+    sdv = dv.sum(0)
+    sdo = dod.float().sum(0).view(cfg.num_kv_heads, g, -1).sum(1)
+    rk = float((sdk.abs() / dk.abs().sum(0)).max())
+    rv = float(((sdv - sdo).abs() / dv.abs().sum(0)).max())
+    log(f"config 3 shape: max |sum dK| / sum|dK| = {rk:.3e}, "
+        f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
+    assert rk <= 1e-2 and rv <= 1e-2
+    rows = np.asarray(sample_rows(cfg, cfg.nq, n_random=16))
+    qpos = problem_positions(prob, cfg.q_idx)
+    kpos = problem_positions(prob, cfg.kv_idx)
+    scale = float(prob["softmax_scale"])
+    for h in (0, 29):
+        hk = h // g
+        f64 = lambda t: t.double().numpy()
+        qh, doh = f64(q[rows, h]), f64(do[rows, h])
+        kh, vh = f64(k[:, hk]), f64(v[:, hk])
+        oh, lh = attention_rows(qh, kh, vh, qpos[rows], kpos, False, scale)
+        D = np.sum(doh * oh, axis=1)
+        rdq, _, _ = attention_rows_bwd(qh, kh, vh, doh, lh, D, qpos[rows],
+                                       kpos, False, scale)
+        got = to_np(dq[torch.as_tensor(rows, device=gpu), h])
+        check_grad(f"config 3 shape dq head {h} ({len(rows)} rows)", got, rdq)
