@@ -17,9 +17,10 @@ resident in HBM:
 `value` is the forward tile TFLOP/s: algorithmic FLOPs of the tile
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
 duration over the timed steps, measured with HIP events on the launch stream.
-`ms_per_step` is the whole step.  Per-stage figures are under `legs` (the
-forward's also gives the host time of building the tile's work list, which
-the library caches and which is outside the timed steps).
+`ms_per_step` is the whole step.  Per-stage figures are under `legs` (mean
+and median over the timed steps; the forward's also gives the host time of
+building the tile's work list, which the library caches and which is outside
+the timed steps).
 Prints one JSON line on stdout; progress goes to stderr.
 """
 
@@ -283,8 +284,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    leg_ms = {n: sum(e[n][0].elapsed_time(e[n][1]) for e in events) /
-              args.steps for n in legs}
+    leg_times = {n: sorted(e[n][0].elapsed_time(e[n][1]) for e in events)
+                 for n in legs}
+    leg_ms = {n: sum(t) / args.steps for n, t in leg_times.items()}
+    leg_med = {n: (t[(len(t) - 1) // 2] + t[len(t) // 2]) / 2
+               for n, t in leg_times.items()}
     log(f"step {ms_step:.3f} ms; " +
         ", ".join(f"{n} {leg_ms[n]:.3f} ms" for n in legs))
 
@@ -312,6 +316,7 @@ def main():
                     "kernel": "tile_fwd_kernel<128,bf16 out>",
                     "flop_per_launch": fwd_flop}
         out_legs["fwd"] = {"ms": round(leg_ms["fwd"], 4),
+                           "ms_median": round(leg_med["fwd"], 4),
                            "tflops": round(tf, 2),
                            "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
                            "flop": fwd_flop,
@@ -320,6 +325,7 @@ def main():
     if "chunks" in legs:
         tc = fwd_flop / (leg_ms["chunks"] * 1e-3) / 1e12
         out_legs["chunks"] = {"ms": round(leg_ms["chunks"], 4),
+                              "ms_median": round(leg_med["chunks"], 4),
                               "tflops": round(tc, 2),
                               "frac_bf16_peak": round(tc / PEAK_BF16_TFLOPS,
                                                       4),
@@ -330,6 +336,7 @@ def main():
         gbs = mbytes / (leg_ms["merge"] * 1e-3) / 1e9
         mdig = source_digest(["lse_merge.hip", "internal.h"])
         out_legs["merge"] = {"ms": round(leg_ms["merge"], 4),
+                             "ms_median": round(leg_med["merge"], 4),
                              "traffic": load_traffic("lse_merge", mdig),
                              "GB/s": round(gbs, 1),
                              "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
@@ -339,6 +346,7 @@ def main():
     if "bwd" in legs:
         tb = bwd_flop / (leg_ms["bwd"] * 1e-3) / 1e12
         out_legs["bwd"] = {"ms": round(leg_ms["bwd"], 4),
+                           "ms_median": round(leg_med["bwd"], 4),
                            "tflops": round(tb, 2),
                            "frac_bf16_peak": round(tb / PEAK_BF16_TFLOPS, 4),
                            "flop": bwd_flop}
