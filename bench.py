@@ -150,13 +150,16 @@ def main():
                          "tasks, see --chunks)")
     ap.add_argument("--chunks", default="4x4",
                     help="k_Q x k_KV of the chunks leg")
-    ap.add_argument("--workload", type=int, default=2,
-                    choices=(2, 3, 4, 6, 7),
-                    help="forward tile: 2 causal 64K (default), 3 1M-token "
-                         "non-causal GQA 16x16 tile, 4 1M-token causal 16x16 "
-                         "tile with outliers, 6 striped causal 64K, 7 "
-                         "striped 1M-token causal 16x16 tile (the backward "
-                         "leg runs on 2 and 6 only)")
+    ap.add_argument("--workload", default="causal-64k",
+                    choices=("causal-64k", "mesh1m-nc-gqa",
+                             "mesh1m-causal-outlier", "striped-causal-64k",
+                             "striped-mesh1m-causal"),
+                    help="forward tile: causal-64k (default), mesh1m-nc-gqa "
+                         "(1M-token non-causal GQA 16x16 tile), "
+                         "mesh1m-causal-outlier (1M-token causal 16x16 tile "
+                         "with outliers), striped-causal-64k, "
+                         "striped-mesh1m-causal; the backward leg runs on "
+                         "the two 64K tiles only")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -165,20 +168,21 @@ def main():
                          "counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for "
-              f"--gpus {args.gpus}); the multi-GPU mesh is not built.",
+        print(f"bench.py: the library runs on one GPU (asked for "
+              f"--gpus {args.gpus}); the multi-GPU mesh is not implemented.",
               file=sys.stderr)
         sys.exit(2)
     legs = [x for x in args.legs.split(",") if x]
 
     import torch
     import paper_2512_20968_amd as ma
-    from mesh_inputs import CONFIGS, make_grad, make_merge_parts, make_qkv
+    from mesh_inputs import WORKLOADS, make_grad, make_merge_parts, make_qkv
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg = CONFIGS[args.workload]
-    if "bwd" in legs and args.workload not in (2, 6):
+    cfg = WORKLOADS[args.workload]
+    if "bwd" in legs and args.workload not in ("causal-64k",
+                                               "striped-causal-64k"):
         legs.remove("bwd")
     prob = cfg.problem()
     P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
@@ -193,9 +197,10 @@ def main():
     ws_f = torch.empty(ma.mesh_attn_fwd_workspace_size(prob, cfg.nq, cfg.nkv),
                        dtype=torch.uint8, device=dev)
     if "bwd" in legs:
-        # dO of the backward workload of this tile (config 5 is the
-        # backward of config 2; config 6 carries its own gradient seed).
-        do = make_grad(CONFIGS[5] if args.workload == 2 else cfg).to(dev)
+        # dO of the backward workload of this tile (bwd-causal-64k is the
+        # backward of causal-64k; the striped tile carries its own seed).
+        do = make_grad(WORKLOADS["bwd-causal-64k"]
+                       if args.workload == "causal-64k" else cfg).to(dev)
         dq = torch.empty((rq, hq, d), dtype=torch.float32, device=dev)
         dk = torch.empty((rkv, hkv, d), dtype=torch.float32, device=dev)
         dv = torch.empty_like(dk)

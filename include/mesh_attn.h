@@ -49,7 +49,7 @@ extern "C" {
 typedef enum {
   MA_OK = 0,
   MA_ERR_INVALID_ARG = 1,         /* bad size, index, flag or pointer */
-  MA_ERR_UNSUPPORTED = 2,         /* valid request this build does not serve */
+  MA_ERR_UNSUPPORTED = 2,         /* valid request the library does not serve */
   MA_ERR_WORKSPACE_TOO_SMALL = 3, /* ws_bytes below the *_workspace_size() */
   MA_ERR_HIP = 4,                 /* HIP runtime error, text in last_error */
   MA_ERR_CAPACITY = 5             /* caller-provided output array too small */

@@ -59,33 +59,40 @@ class TileConfig:
                     layout=self.layout)
 
 
-CONFIGS = {
-    1: TileConfig("tiny-nc", 4, 256, [0, 1], [0, 1], 4, 4, 64, False, seed=0,
-                  note="1024 tokens, 4 partitions of 256, tile {0,1}x{0,1}"),
-    2: TileConfig("causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
-                  32, 32, 128, True, seed=1,
-                  note="65536 tokens, 16 partitions of 4096, tile {4..7}x{0..7}"),
-    3: TileConfig("mesh1m-nc-gqa", 256, 4096, list(range(16, 32)),
-                  list(range(32, 48)), 32, 8, 128, False, seed=2,
-                  note="1M tokens, 256 partitions, 16x16 tile Q16..31 x KV32..47"),
-    4: TileConfig("mesh1m-causal-outlier", 256, 4096, list(range(24, 40)),
-                  list(range(16, 32)), 32, 32, 128, True, seed=3,
-                  outliers=True,
-                  note="1M tokens, 16x16 tile Q24..39 x KV16..31, x8 outlier rows"),
-    5: TileConfig("bwd-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
-                  32, 32, 128, True, seed=1, grad_seed=4,
-                  note="backward of the causal-64k tile; dO from seed 4"),
+# Seeded synthetic workloads, by name.
+WORKLOADS = {
+    "tiny-nc": TileConfig(
+        "tiny-nc", 4, 256, [0, 1], [0, 1], 4, 4, 64, False, seed=0,
+        note="1024 tokens, 4 partitions of 256, tile {0,1}x{0,1}"),
+    "causal-64k": TileConfig(
+        "causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
+        32, 32, 128, True, seed=1,
+        note="65536 tokens, 16 partitions of 4096, tile {4..7}x{0..7}"),
+    "mesh1m-nc-gqa": TileConfig(
+        "mesh1m-nc-gqa", 256, 4096, list(range(16, 32)),
+        list(range(32, 48)), 32, 8, 128, False, seed=2,
+        note="1M tokens, 256 partitions, 16x16 tile Q16..31 x KV32..47"),
+    "mesh1m-causal-outlier": TileConfig(
+        "mesh1m-causal-outlier", 256, 4096, list(range(24, 40)),
+        list(range(16, 32)), 32, 32, 128, True, seed=3, outliers=True,
+        note="1M tokens, 16x16 tile Q24..39 x KV16..31, x8 outlier rows"),
+    "bwd-causal-64k": TileConfig(
+        "bwd-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
+        32, 32, 128, True, seed=1, grad_seed=4,
+        note="backward of the causal-64k tile; dO from seed 4"),
     # Striped layout (token r of partition p at position r*n + p): every
     # partition pair is near-triangular, so every tile of a mesh carries about
     # the same causal work.
-    6: TileConfig("striped-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
-                  32, 32, 128, True, seed=5, grad_seed=6, layout=1,
-                  note="65536 tokens striped over 16 partitions of 4096, "
-                       "tile {4..7}x{0..7}; dO from seed 6"),
-    7: TileConfig("striped-mesh1m-causal", 256, 4096, list(range(24, 40)),
-                  list(range(16, 32)), 32, 32, 128, True, seed=7, layout=1,
-                  note="1M tokens striped over 256 partitions, 16x16 tile "
-                       "Q24..39 x KV16..31"),
+    "striped-causal-64k": TileConfig(
+        "striped-causal-64k", 16, 4096, [4, 5, 6, 7], list(range(8)),
+        32, 32, 128, True, seed=5, grad_seed=6, layout=1,
+        note="65536 tokens striped over 16 partitions of 4096, "
+             "tile {4..7}x{0..7}; dO from seed 6"),
+    "striped-mesh1m-causal": TileConfig(
+        "striped-mesh1m-causal", 256, 4096, list(range(24, 40)),
+        list(range(16, 32)), 32, 32, 128, True, seed=7, layout=1,
+        note="1M tokens striped over 256 partitions, 16x16 tile "
+             "Q24..39 x KV16..31"),
 }
 
 

@@ -12,7 +12,7 @@ import pytest
 
 import bench
 import oracle
-from mesh_inputs import CONFIGS
+from mesh_inputs import WORKLOADS
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -20,7 +20,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.mark.parametrize("layout", [0, 1])
 @pytest.mark.parametrize("causal", [False, True])
 def test_visible_pairs_matches_bruteforce(layout, causal):
-    cfg = dataclasses.replace(CONFIGS[2], num_partitions=6, partition_len=16,
+    cfg = dataclasses.replace(WORKLOADS["causal-64k"], num_partitions=6, partition_len=16,
                               q_idx=[4, 1, 5], kv_idx=[0, 5, 2, 1],
                               causal=causal, layout=layout)
     qpos = oracle.problem_positions(cfg.problem(), cfg.q_idx)
@@ -33,15 +33,15 @@ def test_visible_pairs_matches_bruteforce(layout, causal):
 
 
 def test_visible_pairs_of_the_tile_configs():
-    """Config 2 and config 6 (same tile, contiguous vs striped)."""
+    """causal-64k and striped-causal-64k (same tile, contiguous vs striped)."""
     # causal-64k: 22 full pairs and 4 triangular ones (with their diagonal)
     P = 4096
-    assert bench.visible_pairs(CONFIGS[2]) == 22 * P * P + 4 * P * (P + 1) // 2
+    assert bench.visible_pairs(WORKLOADS["causal-64k"]) == 22 * P * P + 4 * P * (P + 1) // 2
     # striped: 4 x 8 near-triangular pairs; pairs whose KV partition comes
     # after the Q partition lose their diagonal.
-    after = sum(1 for qp in CONFIGS[6].q_idx for kp in CONFIGS[6].kv_idx
+    after = sum(1 for qp in WORKLOADS["striped-causal-64k"].q_idx for kp in WORKLOADS["striped-causal-64k"].kv_idx
                 if kp > qp)
-    assert bench.visible_pairs(CONFIGS[6]) == 32 * P * (P + 1) // 2 - after * P
+    assert bench.visible_pairs(WORKLOADS["striped-causal-64k"]) == 32 * P * (P + 1) // 2 - after * P
 
 
 def test_bench_refuses_more_than_one_gpu():

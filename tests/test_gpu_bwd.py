@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import paper_2512_20968_amd as ma
-from mesh_inputs import CONFIGS, make_grad, make_qkv, sample_rows
+from mesh_inputs import WORKLOADS, make_grad, make_qkv, sample_rows
 
 from helpers import check_grad, log, run_fwd, to_np
 
@@ -64,7 +64,7 @@ MULTI = [
 def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
     """Small tiles (GQA, both head dims, causal and not, permuted lists):
     every row of dQ, dK, dV checked."""
-    cfg = dataclasses.replace(CONFIGS[1], num_partitions=4, partition_len=256,
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], num_partitions=4, partition_len=256,
                               q_idx=q_idx, kv_idx=kv_idx, num_q_heads=hq,
                               num_kv_heads=hkv, head_dim=d, causal=causal,
                               seed=21, grad_seed=22)
@@ -83,7 +83,7 @@ def test_small_tiles_every_row(gpu, q_idx, kv_idx, hq, hkv, d, causal):
 def test_multi_block_partitions_every_row(gpu, q_idx, kv_idx, hq, hkv, d):
     """Causal GQA tile with 1024-token partitions (diagonal pairs spanning
     several blocks, a permuted KV list): every row of dQ, dK, dV."""
-    cfg = dataclasses.replace(CONFIGS[1], num_partitions=3,
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], num_partitions=3,
                               partition_len=1024, q_idx=q_idx, kv_idx=kv_idx,
                               num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                               causal=True, seed=41, grad_seed=42)
@@ -103,7 +103,7 @@ def test_rows_and_keys_nobody_sees(gpu):
     the keys of KV partition 3 are seen by no row.  Their gradient rows must
     be exactly zero (written into uninitialised outputs), every other row
     within tolerance of the oracle."""
-    cfg = dataclasses.replace(CONFIGS[1], num_partitions=4, partition_len=256,
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], num_partitions=4, partition_len=256,
                               q_idx=[0, 2], kv_idx=[1, 3], num_q_heads=4,
                               num_kv_heads=2, head_dim=128, causal=True,
                               seed=21, grad_seed=22)
@@ -126,7 +126,7 @@ def test_rows_and_keys_nobody_sees(gpu):
 
 
 def test_accumulate_adds_into_outputs(gpu):
-    cfg = dataclasses.replace(CONFIGS[1], causal=True, seed=31, grad_seed=32)
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], causal=True, seed=31, grad_seed=32)
     prob, _, (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
     g1 = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     init = tuple(torch.randn_like(t) for t in g1)
@@ -137,7 +137,7 @@ def test_accumulate_adds_into_outputs(gpu):
 
 
 def test_backward_is_deterministic(gpu):
-    cfg = dataclasses.replace(CONFIGS[2], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
+    cfg = dataclasses.replace(WORKLOADS["causal-64k"], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
                               partition_len=1024, num_q_heads=8,
                               num_kv_heads=8, grad_seed=4)
     prob, _, (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
@@ -148,15 +148,15 @@ def test_backward_is_deterministic(gpu):
         assert torch.equal(x, y)
 
 
-def test_config5_backward_causal_64k(gpu):
+def test_causal64k_backward_sampled_rows(gpu):
     """Full-size backward of the causal 64K tile.  The oracle runs its own
     float64 forward for every row of three heads, then checks dQ on the
     sampled Q rows and dK, dV on sampled KV rows of those heads.  On all
     heads, two identities that hold because the tile holds every key the Q
     rows can see: sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
-    cfg = CONFIGS[5]
+    cfg = WORKLOADS["bwd-causal-64k"]
     prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
-    log("config 5: GPU backward")
+    log("causal-64k backward: GPU")
     dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     torch.cuda.synchronize()
     # Identities, all heads.  P and dS are rounded to bf16 before the MFMAs
@@ -169,25 +169,25 @@ def test_config5_backward_causal_64k(gpu):
     mass_v = dv.abs().sum(0)
     rk = float((sdk.abs() / mass_k).max())
     rv = float(((sdv - sdo).abs() / mass_v).max())
-    log(f"config 5: max |sum dK| / sum|dK| = {rk:.3e}, "
+    log(f"causal-64k backward: max |sum dK| / sum|dK| = {rk:.3e}, "
         f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
     assert rk <= 1e-2 and rv <= 1e-2
     heads = [0, 17, 31]
     q_rows = sample_rows(cfg, cfg.nq)
     kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000)
-    log(f"config 5: oracle on heads {heads}, {len(q_rows)} dQ rows, "
+    log(f"causal-64k backward: oracle on heads {heads}, {len(q_rows)} dQ rows, "
         f"{len(kv_rows)} dK/dV rows")
     rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
         prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do),
         kv_heads=heads, q_rows=q_rows, kv_rows=kv_rows)
     qr = torch.tensor(q_rows, device=gpu)
     kr = torch.tensor(kv_rows, device=gpu)
-    check_grad("config 5 dq", to_np(dq[qr][:, q_heads]), rdq)
-    check_grad("config 5 dk", to_np(dk[kr][:, heads]), rdk)
-    check_grad("config 5 dv", to_np(dv[kr][:, heads]), rdv)
+    check_grad("causal-64k dq", to_np(dq[qr][:, q_heads]), rdq)
+    check_grad("causal-64k dk", to_np(dk[kr][:, heads]), rdk)
+    check_grad("causal-64k dv", to_np(dv[kr][:, heads]), rdv)
 
 
-def test_config3_shape_gqa_backward(gpu):
+def test_mesh1m_gqa_backward_full_size(gpu):
     """Backward at the 1M-token non-causal GQA tile's full size (65536 rows,
     32 query heads on 8 KV heads).  dQ of sampled rows of two query heads (in
     different KV groups) against the float64 definition on those rows; on
@@ -196,9 +196,9 @@ def test_config3_shape_gqa_backward(gpu):
     over the rows and the query heads of the group."""
     from oracle.attention import (attention_rows, attention_rows_bwd,
                                   problem_positions)
-    cfg = dataclasses.replace(CONFIGS[3], grad_seed=8)
+    cfg = dataclasses.replace(WORKLOADS["mesh1m-nc-gqa"], grad_seed=8)
     prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
-    log("config 3 shape: GPU backward")
+    log("mesh1m-nc-gqa backward: GPU")
     dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     torch.cuda.synchronize()
     g = cfg.num_q_heads // cfg.num_kv_heads
@@ -207,7 +207,7 @@ def test_config3_shape_gqa_backward(gpu):
     sdo = dod.float().sum(0).view(cfg.num_kv_heads, g, -1).sum(1)
     rk = float((sdk.abs() / dk.abs().sum(0)).max())
     rv = float(((sdv - sdo).abs() / dv.abs().sum(0)).max())
-    log(f"config 3 shape: max |sum dK| / sum|dK| = {rk:.3e}, "
+    log(f"mesh1m-nc-gqa backward: max |sum dK| / sum|dK| = {rk:.3e}, "
         f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
     assert rk <= 1e-2 and rv <= 1e-2
     rows = np.asarray(sample_rows(cfg, cfg.nq, n_random=16))
@@ -224,4 +224,4 @@ def test_config3_shape_gqa_backward(gpu):
         rdq, _, _ = attention_rows_bwd(qh, kh, vh, doh, lh, D, qpos[rows],
                                        kpos, False, scale)
         got = to_np(dq[torch.as_tensor(rows, device=gpu), h])
-        check_grad(f"config 3 shape dq head {h} ({len(rows)} rows)", got, rdq)
+        check_grad(f"mesh1m-nc-gqa dq head {h} ({len(rows)} rows)", got, rdq)

@@ -2,8 +2,8 @@
 sampled-row tests cover them by default).  Opt-in: the oracle's full forward
 takes minutes of host time (causal 64K: 8.8 TFLOP in float64, ~75 s on 16
 cores; the 1M-token tiles about eight times that), so it runs only with
-MESH_ATTN_FULL_TILE set to a comma list of workload ids (e.g. "2" or
-"2,3,4")."""
+MESH_ATTN_FULL_TILE set to a comma list of workload names (e.g.
+"causal-64k" or "causal-64k,mesh1m-nc-gqa,mesh1m-causal-outlier")."""
 
 import os
 import time
@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle
-from mesh_inputs import CONFIGS, make_qkv
+from mesh_inputs import WORKLOADS, make_qkv
 
 from helpers import check_fwd, log, run_fwd, to_np
 
@@ -21,16 +21,17 @@ pytestmark = [
     pytest.mark.gpu,
     pytest.mark.skipif(not os.environ.get("MESH_ATTN_FULL_TILE"),
                        reason="full-tile oracle run is opt-in "
-                              "(MESH_ATTN_FULL_TILE=2,3,4)"),
+                              "(MESH_ATTN_FULL_TILE=<workload names>)"),
 ]
 
 
-@pytest.mark.parametrize("cid", [2, 3, 4])
-def test_every_row_every_head(gpu, cid):
+@pytest.mark.parametrize(
+    "name", ["causal-64k", "mesh1m-nc-gqa", "mesh1m-causal-outlier"])
+def test_every_row_every_head(gpu, name):
     wanted = os.environ.get("MESH_ATTN_FULL_TILE", "").split(",")
-    if str(cid) not in wanted:
-        pytest.skip(f"workload {cid} not selected")
-    cfg = CONFIGS[cid]
+    if name not in wanted:
+        pytest.skip(f"workload {name} not selected")
+    cfg = WORKLOADS[name]
     q, k, v, _ = make_qkv(cfg)
     qd, kd, vd = (t.to(gpu) for t in (q, k, v))
     o, lse = run_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx, qd, kd, vd)
@@ -42,10 +43,10 @@ def test_every_row_every_head(gpu, cid):
     for h in range(cfg.num_q_heads):
         ro, rl = oracle.tile_forward(cfg.problem(), cfg.q_idx, cfg.kv_idx, qn,
                                      kn, vn, heads=[h])
-        eo, el = check_fwd(f"config {cid} head {h} (all {ro.shape[0]} rows)",
+        eo, el = check_fwd(f"{name} head {h} (all {ro.shape[0]} rows)",
                            og[:, h:h + 1], lg[h:h + 1], ro, rl)
         worst_o, worst_l = max(worst_o, eo), max(worst_l, el)
         log(f"  head {h} done, {time.time() - t0:.0f} s")
-    log(f"config {cid}, every row and head: max|O err| {worst_o:.3e}, "
+    log(f"{name}, every row and head: max|O err| {worst_o:.3e}, "
         f"max|LSE err| {worst_l:.3e}")
     assert np.isfinite(worst_o) and np.isfinite(worst_l)

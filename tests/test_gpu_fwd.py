@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import paper_2512_20968_amd as ma
-from mesh_inputs import CONFIGS, make_merge_parts, make_qkv, sample_rows
+from mesh_inputs import WORKLOADS, make_merge_parts, make_qkv, sample_rows
 
 from helpers import check_fwd, log, run_fwd, to_np
 
@@ -28,10 +28,10 @@ def _problem(cfg, **kw):
 
 
 @pytest.mark.parametrize("causal", [0, 1])
-def test_config1_full_tile_fused_and_split_merge(gpu, causal):
+def test_tiny_tile_fused_and_split_merge(gpu, causal):
     """Tiny tile {0,1} x {0,1}: every row checked, by the fused call and by one
     call per KV partition (float32 partials) folded by the merge kernel."""
-    cfg = CONFIGS[1]
+    cfg = WORKLOADS["tiny-nc"]
     prob = _problem(cfg, causal=causal)
     (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
     P = cfg.partition_len
@@ -60,11 +60,11 @@ def test_config1_full_tile_fused_and_split_merge(gpu, causal):
                   to_np(pl[b]), rpo, rpl)
 
 
-def test_config1_convex_combination(gpu):
+def test_tiny_tile_convex_combination(gpu):
     """Every output row is a convex combination of V rows: per channel it lies
     within [min_j v_j, max_j v_j] over the visible keys (up to bf16 rounding of
     the output)."""
-    cfg = CONFIGS[1]
+    cfg = WORKLOADS["tiny-nc"]
     prob = _problem(cfg, causal=1)
     (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
     o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, torch.float32)
@@ -101,28 +101,28 @@ def _sampled_parity(cfg, gpu, rows_extra=None, heads=None):
     return o, lse
 
 
-def test_config2_causal_64k(gpu):
-    _sampled_parity(CONFIGS[2], gpu)
+def test_causal64k_sampled(gpu):
+    _sampled_parity(WORKLOADS["causal-64k"], gpu)
 
 
-def test_config3_mesh1m_noncausal_gqa(gpu):
-    _sampled_parity(CONFIGS[3], gpu)
+def test_mesh1m_nc_gqa_sampled(gpu):
+    _sampled_parity(WORKLOADS["mesh1m-nc-gqa"], gpu)
 
 
-def test_config4_mesh1m_causal_outliers(gpu):
-    _sampled_parity(CONFIGS[4], gpu)
+def test_mesh1m_causal_outlier_sampled(gpu):
+    _sampled_parity(WORKLOADS["mesh1m-causal-outlier"], gpu)
 
 
 def test_tile_above_diagonal_has_no_visible_key(gpu):
     """Causal tile whose KV partitions all lie after its Q partitions: every
     row sees nothing, O = 0 and LSE = -inf.  A mixed tile keeps both kinds."""
-    cfg = dataclasses.replace(CONFIGS[1], q_idx=[0, 1], kv_idx=[2, 3], seed=5)
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], q_idx=[0, 1], kv_idx=[2, 3], seed=5)
     (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
     prob = _problem(cfg, causal=1)
     o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
     torch.cuda.synchronize()
     assert torch.all(o == 0) and torch.all(torch.isneginf(lse))
-    cfg2 = dataclasses.replace(CONFIGS[1], q_idx=[0, 3], kv_idx=[2, 1], seed=6)
+    cfg2 = dataclasses.replace(WORKLOADS["tiny-nc"], q_idx=[0, 3], kv_idx=[2, 1], seed=6)
     (q, k, v), (qd, kd, vd), _ = _inputs(cfg2, gpu)
     o, lse = run_fwd(prob, cfg2.q_idx, cfg2.kv_idx, qd, kd, vd)
     torch.cuda.synchronize()
@@ -137,7 +137,7 @@ def test_kvr_strided_list_gqa_causal(gpu, d, hq, hkv):
     """Strided, non-contiguous KV footprint as KV Partition Rotation produces
     (c + t*a), several Q partitions spanning the diagonal, GQA, both head dims;
     every row checked."""
-    cfg = dataclasses.replace(CONFIGS[1], num_partitions=9, partition_len=256,
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], num_partitions=9, partition_len=256,
                               q_idx=[3, 4, 5], kv_idx=[1, 4, 7],
                               num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                               causal=True, seed=9)
@@ -151,7 +151,7 @@ def test_kvr_strided_list_gqa_causal(gpu, d, hq, hkv):
 
 
 def test_forward_is_deterministic(gpu):
-    cfg = dataclasses.replace(CONFIGS[2], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
+    cfg = dataclasses.replace(WORKLOADS["causal-64k"], q_idx=[6, 7], kv_idx=[0, 5, 6, 7],
                               partition_len=1024, num_q_heads=8,
                               num_kv_heads=8)
     (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
@@ -167,7 +167,7 @@ def test_multi_block_partitions_every_row(gpu, d, hq, hkv):
     """1024-token partitions (four 256-row Q blocks and sixteen 64-key blocks
     per partition, so diagonal pairs mix FULL, PARTIAL and EMPTY blocks),
     causal GQA, permuted lists, both head dims: every row checked."""
-    cfg = dataclasses.replace(CONFIGS[1], num_partitions=3,
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], num_partitions=3,
                               partition_len=1024, q_idx=[2, 1],
                               kv_idx=[0, 2, 1], num_q_heads=hq,
                               num_kv_heads=hkv, head_dim=d, causal=True,

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import paper_2512_20968_amd as ma
-from mesh_inputs import CONFIGS, make_qkv, sample_rows
+from mesh_inputs import WORKLOADS, make_qkv, sample_rows
 from oracle import goo
 
 from helpers import check_fwd, check_grad, log, run_fwd, to_np
@@ -54,7 +54,7 @@ def _small(layout, **kw):
                 kv_idx=[0, 1, 2, 3], num_q_heads=4, num_kv_heads=2,
                 head_dim=128, causal=True, seed=51, layout=layout)
     base.update(kw)
-    return dataclasses.replace(CONFIGS[1], **base)
+    return dataclasses.replace(WORKLOADS["tiny-nc"], **base)
 
 
 @pytest.mark.parametrize("layout", [0, 1])
@@ -107,15 +107,15 @@ def test_accumulated_chunks_equal_the_tile(gpu, layout, kq, kkv):
                   to_np(fo)[r], to_np(fl)[:, r])
 
 
-def test_config2_in_4x4_chunk_tasks(gpu):
+def test_causal64k_in_4x4_chunk_tasks(gpu):
     """The causal 64K tile as 16 chunk tasks: sampled rows against the
     oracle, all rows against the fused kernel."""
-    cfg = CONFIGS[2]
+    cfg = WORKLOADS["causal-64k"]
     kq = kkv = 4
     q, k, v, _ = make_qkv(cfg)
     qd, kd, vd = (t.to(gpu) for t in (q, k, v))
     order = [(i, j) for i in range(kq) for j in range(kkv)]
-    log("config 2: 16 chunk tasks")
+    log("causal-64k: 16 chunk tasks")
     out = _run_chunks(cfg, qd, kd, vd, kq, kkv, order)
     fo, fl = run_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx, qd, kd, vd,
                      torch.float32)
@@ -127,7 +127,7 @@ def test_config2_in_4x4_chunk_tasks(gpu):
         r = _rows(P, cfg.nq, kq, i, gpu)
         o_all[r] = out[i][0]
         l_all[:, r] = out[i][1]
-    check_fwd("config 2 as 4x4 chunks vs fused (all rows)", to_np(o_all),
+    check_fwd("causal-64k as 4x4 chunks vs fused (all rows)", to_np(o_all),
               to_np(l_all), to_np(fo).astype(np.float64),
               to_np(fl).astype(np.float64))
     rows = sample_rows(cfg, cfg.nq, n_random=16)
@@ -136,7 +136,7 @@ def test_config2_in_4x4_chunk_tasks(gpu):
                                  to_np(q), to_np(k), to_np(v), rows=rows,
                                  heads=heads)
     rr = torch.tensor(rows, device=gpu)
-    check_fwd("config 2 as 4x4 chunks", to_np(o_all[rr][:, heads]),
+    check_fwd("causal-64k as 4x4 chunks", to_np(o_all[rr][:, heads]),
               to_np(l_all[heads][:, rr]), ro, rl)
 
 
@@ -193,13 +193,13 @@ def test_chunk_backward_sums_to_the_tile(gpu, layout, kq, kkv):
     check_grad(f"{tag} C-{i}-{j} dv", to_np(gv), cv)
 
 
-def test_config5_backward_as_2x2_chunk_tasks(gpu):
+def test_causal64k_backward_as_2x2_chunk_tasks(gpu):
     """The full-size causal 64K backward as 2 x 2 chunk tasks accumulated into
     zeroed gradients: every row against the fused tile backward (itself
     checked against the oracle in test_gpu_bwd), within the summation-order
     tolerance of the gradients."""
     from mesh_inputs import make_grad
-    cfg = CONFIGS[5]
+    cfg = WORKLOADS["bwd-causal-64k"]
     q, k, v, _ = make_qkv(cfg)
     do = make_grad(cfg)
     qd, kd, vd, dod = (t.to(gpu) for t in (q, k, v, do))
@@ -216,7 +216,7 @@ def test_config5_backward_as_2x2_chunk_tasks(gpu):
     dq = torch.zeros_like(fdq)
     dk = torch.zeros_like(fdk)
     dv = torch.zeros_like(fdk)
-    log("config 5: backward as 2x2 chunk tasks")
+    log("causal-64k backward as 2x2 chunk tasks")
     for i in range(kq):
         qr = _rows(P, cfg.nq, kq, i, gpu)
         qc, oc, doc = (t[qr].contiguous() for t in (qd, o, dod))
@@ -239,7 +239,7 @@ def test_config5_backward_as_2x2_chunk_tasks(gpu):
     for name, got, ref in (("dq", dq, fdq), ("dk", dk, fdk), ("dv", dv, fdv)):
         err = float((got - ref).abs().max())
         scale = float(ref.abs().max())
-        log(f"config 5 chunks vs fused {name}: max err {err:.3e}, "
+        log(f"causal-64k chunks vs fused {name}: max err {err:.3e}, "
             f"max |{name}| {scale:.3e}")
         # same products, different fp32 summation order across the chunks
         assert err <= 1e-3 * scale, name

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_2512_20968_amd as ma
-from mesh_inputs import CONFIGS, make_grad, make_qkv, sample_rows
+from mesh_inputs import WORKLOADS, make_grad, make_qkv, sample_rows
 
 from helpers import check_fwd, check_grad, log, run_fwd, to_np
 
@@ -24,7 +24,7 @@ def _cfg(**kw):
                 kv_idx=[1, 3, 0, 2], num_q_heads=4, num_kv_heads=2,
                 head_dim=64, causal=True, seed=41, grad_seed=42, layout=1)
     base.update(kw)
-    return dataclasses.replace(CONFIGS[1], **base)
+    return dataclasses.replace(WORKLOADS["tiny-nc"], **base)
 
 
 def _inputs(cfg, dev):
@@ -74,16 +74,17 @@ def test_striped_mesh_tiles_every_row(gpu, q_idx, kv_idx):
     check_fwd(f"striped tile {q_idx}x{kv_idx}", to_np(o), to_np(lse), ro, rl)
 
 
-@pytest.mark.parametrize("cid", [6, 7])
-def test_striped_configs_sampled(gpu, cid):
-    cfg = CONFIGS[cid]
+@pytest.mark.parametrize("name", ["striped-causal-64k", "striped-mesh1m-causal"])
+def test_striped_workloads_sampled(gpu, name):
+    cfg = WORKLOADS[name]
     prob = cfg.problem()
     (q, k, v), (qd, kd, vd) = _inputs(cfg, gpu)
     log(f"{cfg.name}: launching forward")
     o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
     torch.cuda.synchronize()
     rows = sample_rows(cfg, cfg.nq)
-    heads = list(range(cfg.num_q_heads)) if cid == 6 else [0, 13, 31]
+    heads = (list(range(cfg.num_q_heads)) if name == "striped-causal-64k"
+             else [0, 13, 31])
     log(f"{cfg.name}: oracle on {len(rows)} rows x {len(heads)} heads")
     ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, to_np(q),
                                  to_np(k), to_np(v), rows=rows, heads=heads)
@@ -126,28 +127,28 @@ def test_striped_backward_every_row(gpu, q_idx, kv_idx, d, hq, hkv):
     check_grad(f"{tag} dv", to_np(dv), rdv)
 
 
-def test_config6_striped_backward_sampled(gpu):
+def test_striped_causal64k_backward_sampled(gpu):
     """Full-size backward of the striped 64K tile; the oracle checks two
     heads on sampled rows (its forward covers every row of those heads)."""
-    cfg = CONFIGS[6]
+    cfg = WORKLOADS["striped-causal-64k"]
     prob = cfg.problem()
     (q, k, v), (qd, kd, vd) = _inputs(cfg, gpu)
     do = make_grad(cfg)
     dod = do.to(gpu)
     o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
-    log("config 6: GPU backward")
+    log("striped-causal-64k: GPU backward")
     dq, dk, dv = _bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     torch.cuda.synchronize()
     heads = [3, 30]
     q_rows = sample_rows(cfg, cfg.nq, n_random=16)
     kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000, n_random=16)
-    log(f"config 6: oracle on heads {heads}, {len(q_rows)} dQ rows, "
+    log(f"striped-causal-64k: oracle on heads {heads}, {len(q_rows)} dQ rows, "
         f"{len(kv_rows)} dK/dV rows")
     rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
         prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do),
         kv_heads=heads, q_rows=q_rows, kv_rows=kv_rows)
     qr = torch.tensor(q_rows, device=gpu)
     kr = torch.tensor(kv_rows, device=gpu)
-    check_grad("config 6 dq", to_np(dq[qr][:, q_heads]), rdq)
-    check_grad("config 6 dk", to_np(dk[kr][:, heads]), rdk)
-    check_grad("config 6 dv", to_np(dv[kr][:, heads]), rdv)
+    check_grad("striped-causal-64k dq", to_np(dq[qr][:, q_heads]), rdq)
+    check_grad("striped-causal-64k dk", to_np(dk[kr][:, heads]), rdk)
+    check_grad("striped-causal-64k dv", to_np(dv[kr][:, heads]), rdv)

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import paper_2512_20968_amd as ma
-from mesh_inputs import CONFIGS
+from mesh_inputs import WORKLOADS
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -59,10 +59,10 @@ def _check_bitexact(prob, q_idx, kv_idx, bm, bn):
     np.testing.assert_array_equal(runs, want_runs)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("name", list(WORKLOADS))
 @pytest.mark.parametrize("pass_", [0, 1])
-def test_worklist_bitexact_on_configs(cid, pass_):
-    cfg = CONFIGS[cid]
+def test_worklist_bitexact_on_workloads(name, pass_):
+    cfg = WORKLOADS[name]
     bm, bn = ma.mesh_attn_block_shape(cfg.head_dim, pass_)
     _check_bitexact(cfg.problem(), cfg.q_idx, cfg.kv_idx, bm, bn)
 

@@ -9,7 +9,7 @@ import os
 import numpy as np
 import pytest
 
-from mesh_inputs import CONFIGS
+from mesh_inputs import WORKLOADS
 from oracle import (EMPTY, FULL, PARTIAL, basic_tile, classify_blocks,
                     classify_blocks_bruteforce, kv_major_run_list, kvr_tile,
                     run_list)
@@ -26,10 +26,11 @@ def _pair_counts(q_idx, kv_idx):
     return full, diag, empty
 
 
-@pytest.mark.parametrize("cid,expect", [(1, None), (2, (22, 4, 6)),
-                                        (3, None), (4, (220, 8, 28))])
-def test_partition_pair_classes(cid, expect):
-    cfg = CONFIGS[cid]
+@pytest.mark.parametrize("name,expect", [
+    ("tiny-nc", None), ("causal-64k", (22, 4, 6)), ("mesh1m-nc-gqa", None),
+    ("mesh1m-causal-outlier", (220, 8, 28))])
+def test_partition_pair_classes(name, expect):
+    cfg = WORKLOADS[name]
     P, bm, bn = cfg.partition_len, 128, 64
     cls = classify_blocks(cfg.q_idx, cfg.kv_idx, P, bm, bn, cfg.causal)
     nqb, nkb = P // bm, P // bn
@@ -75,9 +76,9 @@ def test_diagonal_pair_closed_form(bm, bn):
             assert np.all(row[rho * qb + rho:] == EMPTY)
 
 
-@pytest.mark.parametrize("cid", [1, 2, 5])
-def test_block_classes_match_bruteforce_on_configs(cid):
-    cfg = CONFIGS[cid]
+@pytest.mark.parametrize("name", ["tiny-nc", "causal-64k", "bwd-causal-64k"])
+def test_block_classes_match_bruteforce_on_workloads(name):
+    cfg = WORKLOADS[name]
     args = (cfg.q_idx, cfg.kv_idx, cfg.partition_len, 128, 64, cfg.causal)
     np.testing.assert_array_equal(classify_blocks(*args),
                                   classify_blocks_bruteforce(*args))
@@ -116,7 +117,7 @@ def test_run_list_hand_fixture():
 
 
 def test_run_list_covers_exactly_the_non_empty_blocks():
-    cfg = CONFIGS[4]
+    cfg = WORKLOADS["mesh1m-causal-outlier"]
     P, bm, bn = cfg.partition_len, 128, 64
     cls = classify_blocks(cfg.q_idx, cfg.kv_idx, P, bm, bn, True)
     nkb = P // bn
@@ -140,5 +141,5 @@ def test_paper_footprint_examples():
 
 def test_config_tiles_are_mesh_tiles():
     """The 1M-token non-causal tile is GPU 18 of a 16x16 basic tiling."""
-    cfg = CONFIGS[3]
+    cfg = WORKLOADS["mesh1m-nc-gqa"]
     assert basic_tile(18, 16, 16) == (cfg.q_idx, cfg.kv_idx)
