@@ -12,9 +12,10 @@
  *
  * Conventions shared by every call
  * --------------------------------
- *  - The sequence of num_partitions * partition_len tokens is split into
- *    contiguous partitions of partition_len (P) tokens.  Token r of partition
- *    p has global position p * P + r; the causal rule (Section 3.7) lets a
+ *  - The sequence of num_partitions (n) * partition_len (P) tokens is split
+ *    into n partitions of P tokens.  The problem's layout fixes the global
+ *    position of token r of partition p: p * P + r (MA_LAYOUT_CONTIGUOUS) or
+ *    r * n + p (MA_LAYOUT_STRIPED).  The causal rule (Section 3.7) lets a
  *    query see a key iff key position <= query position.
  *  - A tile buffer stacks its partitions in the order of its index list: row
  *    a * P + r of the Q buffer is token r of partition q_idx[a] (the order an
@@ -26,9 +27,11 @@
  *    num_kv_heads).
  *  - Device pointers must be 16-byte aligned.  Outputs must not alias inputs.
  *  - The caller owns every buffer, host and device.  The library never
- *    allocates or frees device memory and never synchronizes the stream; a
- *    small process-lifetime cache of pinned host copies of work lists is its
- *    only state (guarded by a mutex).
+ *    allocates or frees device memory and never synchronizes a stream or the
+ *    device; its only state is a bounded cache of pinned host copies of work
+ *    lists (guarded by a mutex).  A cached copy is released only after the
+ *    device has finished every upload from it (an event recorded after each
+ *    upload, polled without waiting).
  *  - Arguments are validated on the host before anything is enqueued.  On a
  *    non-OK status nothing was launched and mesh_attn_last_error() describes
  *    the problem.  Device work runs asynchronously on `stream`; a launch
@@ -66,7 +69,7 @@ enum { MA_CLS_EMPTY = 0, MA_CLS_PARTIAL = 1, MA_CLS_FULL = 2 };
  *   MA_LAYOUT_STRIPED:    position r * n + p (positions dealt round robin over
  *                         the n partitions, the striped layout Section 3.7
  *                         adopts to balance causal work across tiles). */
-enum { MA_LAYOUT_CONTIGUOUS = 0, MA_LAYOUT_STRIPED = 1 };
+typedef enum { MA_LAYOUT_CONTIGUOUS = 0, MA_LAYOUT_STRIPED = 1 } ma_layout_t;
 
 typedef struct {
   int32_t num_partitions; /* n: partitions of the whole sequence, >= 1        */
@@ -74,10 +77,10 @@ typedef struct {
   int32_t num_q_heads;    /* Hq >= 1                                         */
   int32_t num_kv_heads;   /* Hkv >= 1, divides Hq                            */
   int32_t head_dim;       /* d: 64 or 128                                    */
-  int32_t causal;         /* 0 or 1                                          */
-  float softmax_scale;    /* s > 0, finite; usually 1/sqrt(d)                */
-  int32_t layout;         /* MA_LAYOUT_*; a key is visible to a query iff its
+  int32_t causal;         /* 0 or 1; a key is visible to a query iff its
                              position is not larger (causal problems)        */
+  int32_t layout;         /* an ma_layout_t value                            */
+  float softmax_scale;    /* s > 0, finite; usually 1/sqrt(d)                */
 } ma_problem_t;
 
 /* ---------------------------------------------------------------------------
@@ -105,27 +108,38 @@ ma_status_t mesh_attn_classify(const ma_problem_t* prob, const int32_t* q_idx,
                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
                                int32_t bm, int32_t bn, uint8_t* cls);
 
+/* One run of the work list: the KV blocks [kb_begin, kb_end) of KV list
+ * entry kv_list_pos (blocks counted within that partition) against Q block
+ * qblk (counted in the tile's Q buffer), all of class cls (MA_CLS_PARTIAL or
+ * MA_CLS_FULL).  In the KV-major list the roles of the sides swap (see
+ * mesh_attn_worklist_kv_major). */
+typedef struct {
+  int32_t qblk, kv_list_pos, kb_begin, kb_end, cls;
+} ma_run_t;
+
 /* Canonical Q-major run list.  For every Q block in buffer order, for every
  * KV list entry b in list order, the maximal runs of consecutive KV blocks kb
- * (ascending) of equal class, EMPTY runs dropped.  Each run is five int32
- * (qblk, b, kb_begin, kb_end exclusive, cls) written to runs[5*i..5*i+4];
- * qblk_ptr[q] (nq*P/bm + 1 entries) is the first run of Q block q and its last
- * entry the run count.  cap is the capacity of runs in runs; if it is too
- * small, *n_runs gets the required count and MA_ERR_CAPACITY is returned.  A
- * NULL runs with cap 0 queries the count. */
+ * (ascending) of equal class, EMPTY runs dropped, as ma_run_t
+ * {qblk, b, kb_begin, kb_end exclusive, cls}.  qblk_ptr[q] (nq*P/bm + 1
+ * entries) is the first run of Q block q and its last entry the run count.
+ * cap is the capacity of runs in ma_run_t entries; if it is too small,
+ * *n_runs gets the required count and MA_ERR_CAPACITY is returned.  A NULL
+ * runs with cap 0 queries the count. */
 ma_status_t mesh_attn_worklist(const ma_problem_t* prob, const int32_t* q_idx,
                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
                                int32_t bm, int32_t bn, int32_t* qblk_ptr,
-                               int32_t* runs, int64_t cap, int64_t* n_runs);
+                               ma_run_t* runs, int64_t cap, int64_t* n_runs);
 
 /* KV-major mirror: the same rule with the sides swapped.  For every KV block
- * in buffer order, for every Q list entry a, runs of Q blocks
- * (kvblk, a, qb_begin, qb_end, cls); kvblk_ptr has nkv*P/bn + 1 entries. */
+ * in buffer order, for every Q list entry a, runs of Q blocks; each ma_run_t
+ * then holds {KV block, a, qb_begin, qb_end, cls} in the fields
+ * {qblk, kv_list_pos, kb_begin, kb_end, cls}.  kvblk_ptr has nkv*P/bn + 1
+ * entries. */
 ma_status_t mesh_attn_worklist_kv_major(const ma_problem_t* prob,
                                         const int32_t* q_idx, int32_t nq,
                                         const int32_t* kv_idx, int32_t nkv,
                                         int32_t bm, int32_t bn,
-                                        int32_t* kvblk_ptr, int32_t* runs,
+                                        int32_t* kvblk_ptr, ma_run_t* runs,
                                         int64_t cap, int64_t* n_runs);
 
 /* ---------------------------------------------------------------------------
@@ -236,10 +250,11 @@ typedef struct {
  * deterministic: every GPU of a mesh that calls it with the same shared costs
  * gets the same collective order).  Each step runs one collective and the
  * compute tasks listed for it, all ready when the step starts:
- *   - its collective is, among the lowest-index chunk of each kind that can
- *     run (RS-Q-i once every C-i-j is done), the one with the largest
- *     (time of the compute it makes ready) / (its time); ties go to the one
- *     that makes more compute ready, then to AG-KV, AG-Q, RS-Q in that order;
+ *   - its collective is, among every chunk collective that can run (each
+ *     AG-Q-i and AG-KV-j not yet run, each RS-Q-i not yet run whose C-i-j
+ *     are all done), the one with the largest (time of the compute it makes
+ *     ready) / (its time); ties go to the one that makes more compute ready,
+ *     then to AG-KV, AG-Q, RS-Q in that order, then to the lower chunk index;
  *   - its compute tasks are the ready ones in (i, j) order until their time
  *     reaches gamma times the collective's time;
  *   - when no collective can run, a compute-only step runs one ready task.

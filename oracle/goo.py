@@ -19,12 +19,16 @@ candidate with the highest profit = (time of the compute tasks it would make
 ready) / (its own time); the step is then filled with already-ready compute
 tasks, earliest Q chunk first, until their time reaches gamma * (collective
 time).  When no collective can run but compute is ready, a compute-only step
-runs one task.  Candidates are the lowest-index chunk of each collective type
-that can run (an RS-Q chunk only once all its compute tasks are done).
+runs one task.  Candidates are every chunk collective that can run: each
+AG-Q-i and AG-KV-j not yet scheduled, and each RS-Q-i not yet scheduled whose
+compute tasks are all done.  (The paper's worked example looks only at the
+lowest-index chunk of each type, a simplification it states for that example;
+with equal task costs the general rule picks the same chunks.)
 
 Readings where the paper leaves a choice (the same in the library):
 * ties in profit go to the candidate that makes more compute ready, then to
-  the order AG-KV, AG-Q, RS-Q (the choices of the worked example);
+  the order AG-KV, AG-Q, RS-Q (the choices of the worked example), then to
+  the lower chunk index;
 * among ready compute tasks the order is (Q chunk, KV chunk) ascending;
 * a step's fill stops at the first task that brings the total to the target
   or above (the worked example's steps 3, 4 and 6);
@@ -88,17 +92,10 @@ def goo_plan(k_q, k_kv, t_ag_q, t_ag_kv, t_rs_q, t_c, gamma=1.05):
         return 0.0
 
     while len(ag_q) < k_q or len(ag_kv) < k_kv or len(rs_q) < k_q:
-        cands = []
-        nq = next((i for i in range(k_q) if i not in ag_q), None)
-        if nq is not None:
-            cands.append((AG_Q, nq))
-        nkv = next((j for j in range(k_kv) if j not in ag_kv), None)
-        if nkv is not None:
-            cands.append((AG_KV, nkv))
-        nrs = next((i for i in range(k_q) if i not in rs_q
-                    and all((i, j) in done for j in range(k_kv))), None)
-        if nrs is not None:
-            cands.append((RS_Q, nrs))
+        cands = [(AG_Q, i) for i in range(k_q) if i not in ag_q]
+        cands += [(AG_KV, j) for j in range(k_kv) if j not in ag_kv]
+        cands += [(RS_Q, i) for i in range(k_q) if i not in rs_q
+                  and all((i, j) in done for j in range(k_kv))]
         ready = ready_tasks()
         if not cands:
             # No collective can run: one ready task advances the dependencies.
@@ -109,7 +106,7 @@ def goo_plan(k_q, k_kv, t_ag_q, t_ag_kv, t_rs_q, t_c, gamma=1.05):
         best = None
         for kind, idx in cands:
             u = unlock(kind, idx)
-            key = (u / t_comm[kind], u, -_KIND_ORDER[kind])
+            key = (u / t_comm[kind], u, -_KIND_ORDER[kind], -idx)
             if best is None or key > best[0]:
                 best = (key, kind, idx)
         _, kind, idx = best

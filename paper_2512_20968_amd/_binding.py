@@ -29,24 +29,41 @@ class MeshAttnError(RuntimeError):
         super().__init__(f"{fn}: {_STATUS.get(status, status)}: {text}")
 
 
+MA_LAYOUT_CONTIGUOUS, MA_LAYOUT_STRIPED = 0, 1
+
+
 class Problem(ctypes.Structure):
+    """ma_problem_t."""
     _fields_ = [("num_partitions", ctypes.c_int32),
                 ("partition_len", ctypes.c_int32),
                 ("num_q_heads", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32),
                 ("causal", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float),
-                ("layout", ctypes.c_int32)]
+                ("layout", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
 
     @classmethod
     def make(cls, prob):
         if isinstance(prob, Problem):
             return prob
-        return cls(int(prob["num_partitions"]), int(prob["partition_len"]),
-                   int(prob["num_q_heads"]), int(prob["num_kv_heads"]),
-                   int(prob["head_dim"]), int(prob["causal"]),
-                   float(prob["softmax_scale"]), int(prob.get("layout", 0)))
+        return cls(num_partitions=int(prob["num_partitions"]),
+                   partition_len=int(prob["partition_len"]),
+                   num_q_heads=int(prob["num_q_heads"]),
+                   num_kv_heads=int(prob["num_kv_heads"]),
+                   head_dim=int(prob["head_dim"]),
+                   causal=int(prob["causal"]),
+                   layout=int(prob.get("layout", MA_LAYOUT_CONTIGUOUS)),
+                   softmax_scale=float(prob["softmax_scale"]))
+
+
+class Run(ctypes.Structure):
+    """ma_run_t: one run of the work list."""
+    _fields_ = [("qblk", ctypes.c_int32),
+                ("kv_list_pos", ctypes.c_int32),
+                ("kb_begin", ctypes.c_int32),
+                ("kb_end", ctypes.c_int32),
+                ("cls", ctypes.c_int32)]
 
 
 _lock = threading.Lock()
@@ -84,10 +101,11 @@ _SIGNATURES = {
     "mesh_attn_classify": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _i32, _i32,
                                   _p]),
     "mesh_attn_worklist": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _i32, _i32,
-                                  _I32P, _I32P, _i64,
+                                  _I32P, ctypes.POINTER(Run), _i64,
                                   ctypes.POINTER(ctypes.c_int64)]),
     "mesh_attn_worklist_kv_major": (_i32, [_PROB, _I32P, _i32, _I32P, _i32,
-                                           _i32, _i32, _I32P, _I32P, _i64,
+                                           _i32, _i32, _I32P,
+                                           ctypes.POINTER(Run), _i64,
                                            ctypes.POINTER(ctypes.c_int64)]),
     "mesh_attn_fwd_workspace_size": (_sz, [_PROB, _i32, _i32]),
     "mesh_attn_bwd_workspace_size": (_sz, [_PROB, _i32, _i32]),
@@ -195,11 +213,14 @@ def _worklist(name, prob, q_idx, kv_idx, bm, bn, kv_major):
             ptr.ctypes.data_as(_I32P), None, 0, ctypes.byref(n))
     if st not in (MA_OK, MA_ERR_CAPACITY):
         _check(name, st)
+    # ma_run_t is five int32 without padding: an [n, 5] int32 array has its
+    # layout.
+    assert ctypes.sizeof(Run) == 5 * 4
     runs = np.zeros((n.value, 5), dtype=np.int32)
     st = fn(ctypes.byref(pr), qp, nq, kp, nkv, int(bm), int(bn),
             ptr.ctypes.data_as(_I32P),
-            runs.ctypes.data_as(_I32P) if n.value else None, n.value,
-            ctypes.byref(n))
+            runs.ctypes.data_as(ctypes.POINTER(Run)) if n.value else None,
+            n.value, ctypes.byref(n))
     _check(name, st)
     return ptr, runs
 

@@ -4,10 +4,12 @@
 // k_KV chunks; the chunk collectives are AG-Q-i, AG-KV-j and RS-Q-i, and the
 // compute tasks C-i-j need AG-Q-i and AG-KV-j, while RS-Q-i needs every
 // C-i-j.  The planner emits one step per collective plus compute-only steps:
-//  * the collective of a step is, among the lowest-index chunk of each type
-//    that can run, the one with the largest (time of the compute it makes
-//    ready) / (its own time); ties go to the one that makes more compute
-//    ready, then to AG-KV, AG-Q, RS-Q in that order;
+//  * the collective of a step is, among every chunk collective that can run
+//    (each AG-Q-i and AG-KV-j not yet run, each RS-Q-i not yet run whose
+//    compute tasks are all done), the one with the largest (time of the
+//    compute it makes ready) / (its own time); ties go to the one that makes
+//    more compute ready, then to AG-KV, AG-Q, RS-Q in that order, then to the
+//    lower chunk index;
 //  * the step also runs compute tasks that were ready when it started, in
 //    (Q chunk, KV chunk) order, stopping once their time reaches gamma times
 //    the collective's time;
@@ -35,7 +37,8 @@ struct Cand {
 bool better(const Cand& a, const Cand& b) {  // a strictly preferred to b
   if (a.profit != b.profit) return a.profit > b.profit;
   if (a.unlocked != b.unlocked) return a.unlocked > b.unlocked;
-  return a.rank < b.rank;
+  if (a.rank != b.rank) return a.rank < b.rank;
+  return a.chunk < b.chunk;
 }
 
 }  // namespace
@@ -102,7 +105,6 @@ extern "C" ma_status_t mesh_attn_goo_plan(int32_t k_q, int32_t k_kv,
       c.profit = c.unlocked / t_ag_kv;
       c.rank = 0;
       consider(c);
-      break;
     }
     for (int32_t i = 0; i < k_q; ++i) {
       if (gq[i]) continue;
@@ -114,7 +116,6 @@ extern "C" ma_status_t mesh_attn_goo_plan(int32_t k_q, int32_t k_kv,
       c.profit = c.unlocked / t_ag_q;
       c.rank = 1;
       consider(c);
-      break;
     }
     for (int32_t i = 0; i < k_q; ++i) {
       if (rs[i]) continue;
@@ -126,7 +127,6 @@ extern "C" ma_status_t mesh_attn_goo_plan(int32_t k_q, int32_t k_kv,
       c.chunk = i;
       c.rank = 2;
       consider(c);
-      break;
     }
     if (!have) {
       // Only compute can advance: one ready task, the first in order.

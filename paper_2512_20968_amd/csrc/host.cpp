@@ -213,28 +213,30 @@ void build_runs(const ma_problem_t* p, const int32_t* a_idx, int32_t na,
 
 ma_status_t export_runs(const std::vector<int32_t>& ptr,
                         const std::vector<Run>& runs, int32_t* out_ptr,
-                        int32_t* out_runs, int64_t cap, int64_t* n_runs) {
+                        ma_run_t* out_runs, int64_t cap, int64_t* n_runs) {
   if (n_runs) *n_runs = static_cast<int64_t>(runs.size());
   if (out_ptr) std::memcpy(out_ptr, ptr.data(), ptr.size() * sizeof(int32_t));
   if (static_cast<int64_t>(runs.size()) > cap || (!out_runs && !runs.empty()))
     return fail(MA_ERR_CAPACITY, "run list needs %zu entries, capacity %lld",
                 runs.size(), static_cast<long long>(cap));
-  for (size_t i = 0; i < runs.size(); ++i) {
-    int32_t* r = out_runs + 5 * i;
-    r[0] = runs[i].row;
-    r[1] = runs[i].list;
-    r[2] = runs[i].begin;
-    r[3] = runs[i].end;
-    r[4] = runs[i].cls;
-  }
+  for (size_t i = 0; i < runs.size(); ++i)
+    out_runs[i] = ma_run_t{runs[i].row, runs[i].list, runs[i].begin,
+                           runs[i].end, runs[i].cls};
   return ok();
 }
 
 // ---------------------------------------------------------------------------
 // Device plans: the run list in the kernels' form plus the workgroup order,
 // packed into one pinned host buffer that is copied to the caller's
-// workspace on the caller's stream.  Plans are cached per tile for the life
-// of the process (a pinned source must outlive the asynchronous copy).
+// workspace on the caller's stream.
+//
+// Plans are cached per tile (at most kMaxPlans, least recently used evicted).
+// A pinned source must outlive every asynchronous copy from it, and freeing
+// pinned memory would wait for the device, so buffers are never freed while
+// the library is in use: every upload records an event on the caller's
+// stream, an evicted plan's buffer joins a spare list, and a spare buffer is
+// reused for a new plan only once all events recorded after copies from it
+// have completed (hipEventQuery, which does not wait).  No call synchronizes.
 // ---------------------------------------------------------------------------
 
 constexpr size_t kAlign = 256;
@@ -245,18 +247,69 @@ struct Side {
   int32_t grid = 0;
 };
 
+struct PinnedBuf {
+  void* host = nullptr;
+  size_t cap = 0;
+  std::vector<hipEvent_t> pending;  // recorded after copies from this buffer
+};
+
 struct Plan {
-  void* host = nullptr;  // pinned
+  PinnedBuf* buf = nullptr;
   size_t bytes = 0;
   Side a, b;             // fwd uses a; bwd uses a (Q-major) and b (KV-major)
-  ~Plan() {
-    if (host) (void)hipHostFree(host);
-  }
+  uint64_t last_use = 0;
+};
+
+// What a kernel launch needs from a plan once it is uploaded.
+struct PlanView {
+  size_t bytes = 0;
+  Side a, b;
 };
 
 std::mutex g_plan_mu;
-std::map<std::string, std::shared_ptr<Plan>> g_plans;
+std::map<std::string, Plan> g_plans;
+std::vector<PinnedBuf*> g_spare;       // buffers of evicted plans
+std::vector<hipEvent_t> g_free_events;  // completed events, ready for reuse
+uint64_t g_plan_clock = 0;
 constexpr size_t kMaxPlans = 1024;
+
+// Drops the completed events of `b` (to the free list); true if none remain.
+bool retire_completed(PinnedBuf* b) {
+  size_t keep = 0;
+  for (hipEvent_t ev : b->pending) {
+    if (hipEventQuery(ev) == hipSuccess)
+      g_free_events.push_back(ev);
+    else
+      b->pending[keep++] = ev;
+  }
+  b->pending.resize(keep);
+  return keep == 0;
+}
+
+// A pinned buffer of at least `bytes`: an idle spare if one is large enough
+// (the smallest such), else a new allocation.
+ma_status_t take_buffer(size_t bytes, PinnedBuf** out) {
+  size_t best = g_spare.size();
+  for (size_t i = 0; i < g_spare.size(); ++i) {
+    PinnedBuf* b = g_spare[i];
+    if (b->cap < bytes || !retire_completed(b)) continue;
+    if (best == g_spare.size() || b->cap < g_spare[best]->cap) best = i;
+  }
+  if (best != g_spare.size()) {
+    *out = g_spare[best];
+    g_spare.erase(g_spare.begin() + best);
+    return MA_OK;
+  }
+  auto* b = new PinnedBuf;
+  b->cap = std::max(bytes, kAlign);
+  hipError_t e = hipHostMalloc(&b->host, b->cap, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete b;
+    return hip_fail(e, "hipHostMalloc(work list)");
+  }
+  *out = b;
+  return MA_OK;
+}
 
 std::string plan_key(int pass, const ma_problem_t* p, const int32_t* q_idx,
                      int32_t nq, const int32_t* kv_idx, int32_t nkv,
@@ -385,49 +438,74 @@ size_t side_bound(int64_t n_blocks, int64_t n_list, int64_t heads) {
 
 constexpr ma_chunk_t kWholeTile{0, 1, 0, 1};
 
-ma_status_t get_plan(int pass, const ma_problem_t* p, const int32_t* q_idx,
-                     int32_t nq, const int32_t* kv_idx, int32_t nkv,
-                     const ma_chunk_t& ch, std::shared_ptr<Plan>* out) {
+// Builds (or finds) the plan of a tile, copies it to `ws` on `stream` and
+// records the copy's completion event, all under the cache lock, so that no
+// other thread can recycle the source buffer in between.
+ma_status_t upload_plan(int pass, const ma_problem_t* p, const int32_t* q_idx,
+                        int32_t nq, const int32_t* kv_idx, int32_t nkv,
+                        const ma_chunk_t& ch, void* ws, hipStream_t stream,
+                        PlanView* view) {
   const std::string key = plan_key(pass, p, q_idx, nq, kv_idx, nkv, ch);
   const int64_t P = p->partition_len;
   const Slice sq{P / ch.num_q_chunks, ch.q_chunk * (P / ch.num_q_chunks)};
   const Slice skv{P / ch.num_kv_chunks, ch.kv_chunk * (P / ch.num_kv_chunks)};
   std::lock_guard<std::mutex> lock(g_plan_mu);
   auto it = g_plans.find(key);
-  if (it != g_plans.end()) {
-    *out = it->second;
-    return MA_OK;
+  if (it == g_plans.end()) {
+    const int32_t g = p->num_q_heads / p->num_kv_heads;
+    SideData sa, sb;
+    std::vector<int64_t> work;
+    if (pass == 0) {
+      device_runs(p, q_idx, nq, kFwdBM, sq, kv_idx, nkv, kFwdBN, skv, true,
+                  &sa.ptr, &sa.runs, &work);
+      sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
+    } else {
+      device_runs(p, q_idx, nq, kBwdBM, sq, kv_idx, nkv, kBwdBN, skv, true,
+                  &sa.ptr, &sa.runs, &work);
+      sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
+      device_runs(p, kv_idx, nkv, kBwdBN, skv, q_idx, nq, kBwdBM, sq, false,
+                  &sb.ptr, &sb.runs, &work);
+      sb.order = workgroup_order(work, p->num_kv_heads, 1, p->num_kv_heads);
+    }
+    if (g_plans.size() >= kMaxPlans) {
+      auto lru = g_plans.begin();
+      for (auto i = g_plans.begin(); i != g_plans.end(); ++i)
+        if (i->second.last_use < lru->second.last_use) lru = i;
+      g_spare.push_back(lru->second.buf);
+      g_plans.erase(lru);
+    }
+    Plan plan;
+    plan.bytes = side_bytes(sa) + (pass == 0 ? 0 : side_bytes(sb));
+    ma_status_t st = take_buffer(plan.bytes, &plan.buf);
+    if (st != MA_OK) return st;
+    char* base = static_cast<char*>(plan.buf->host);
+    side_pack(sa, base, 0, &plan.a);
+    if (pass != 0) side_pack(sb, base, side_bytes(sa), &plan.b);
+    it = g_plans.emplace(key, plan).first;
   }
-  const int32_t g = p->num_q_heads / p->num_kv_heads;
-  SideData sa, sb;
-  std::vector<int64_t> work;
-  if (pass == 0) {
-    device_runs(p, q_idx, nq, kFwdBM, sq, kv_idx, nkv, kFwdBN, skv, true,
-                &sa.ptr, &sa.runs, &work);
-    sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
+  Plan& plan = it->second;
+  plan.last_use = ++g_plan_clock;
+  retire_completed(plan.buf);  // keeps the list as short as the copies in flight
+  hipError_t e = hipMemcpyAsync(ws, plan.buf->host, plan.bytes,
+                                hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
+  hipEvent_t ev;
+  if (!g_free_events.empty()) {
+    ev = g_free_events.back();
+    g_free_events.pop_back();
   } else {
-    device_runs(p, q_idx, nq, kBwdBM, sq, kv_idx, nkv, kBwdBN, skv, true,
-                &sa.ptr, &sa.runs, &work);
-    sa.order = workgroup_order(work, p->num_q_heads, g, p->num_kv_heads);
-    device_runs(p, kv_idx, nkv, kBwdBN, skv, q_idx, nq, kBwdBM, sq, false,
-                &sb.ptr, &sb.runs, &work);
-    sb.order = workgroup_order(work, p->num_kv_heads, 1, p->num_kv_heads);
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
   }
-  auto plan = std::make_shared<Plan>();
-  plan->bytes = side_bytes(sa) + (pass == 0 ? 0 : side_bytes(sb));
-  hipError_t e = hipHostMalloc(&plan->host, plan->bytes, hipHostMallocDefault);
-  if (e != hipSuccess) return hip_fail(e, "hipHostMalloc(work list)");
-  char* base = static_cast<char*>(plan->host);
-  side_pack(sa, base, 0, &plan->a);
-  if (pass != 0) side_pack(sb, base, side_bytes(sa), &plan->b);
-  if (g_plans.size() >= kMaxPlans) {
-    // Copies from cached plans may still be queued: drain the device before
-    // releasing their pinned sources.
-    (void)hipDeviceSynchronize();
-    g_plans.clear();
+  e = hipEventRecord(ev, stream);
+  if (e != hipSuccess) {
+    g_free_events.push_back(ev);
+    return hip_fail(e, "hipEventRecord(work list)");
   }
-  g_plans[key] = plan;
-  *out = plan;
+  plan.buf->pending.push_back(ev);
+  view->bytes = plan.bytes;
+  view->a = plan.a;
+  view->b = plan.b;
   return MA_OK;
 }
 
@@ -497,12 +575,9 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   if (ws_bytes < need)
     return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
                 ws_bytes, need);
-  std::shared_ptr<Plan> plan;
-  st = get_plan(0, prob, q_idx, nq, kv_idx, nkv, ch, &plan);
+  PlanView plan;
+  st = upload_plan(0, prob, q_idx, nq, kv_idx, nkv, ch, ws, stream, &plan);
   if (st != MA_OK) return st;
-  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
-                                hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
   char* wsb = static_cast<char*>(ws);
   FwdParams fp{};
   fp.q = static_cast<const uint16_t*>(q);
@@ -510,17 +585,17 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   fp.v = static_cast<const uint16_t*>(v);
   fp.o = o;
   fp.lse = lse;
-  fp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
-  fp.runs = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
-  fp.order = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
+  fp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan.a.off_ptr);
+  fp.runs = reinterpret_cast<const DevRun*>(wsb + plan.a.off_runs);
+  fp.order = reinterpret_cast<const int2*>(wsb + plan.a.off_order);
   fp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
   fp.hq = prob->num_q_heads;
   fp.hkv = prob->num_kv_heads;
   fp.group = prob->num_q_heads / prob->num_kv_heads;
   fp.scale_log2 = prob->softmax_scale * kLog2e;
   fp.accumulate = accumulate;
-  if (plan->a.grid == 0) return ok();  // cannot happen: every block is listed
-  e = launch_tile_fwd(fp, prob->head_dim, o_f32, plan->a.grid, stream);
+  if (plan.a.grid == 0) return ok();  // cannot happen: every block is listed
+  hipError_t e = launch_tile_fwd(fp, prob->head_dim, o_f32, plan.a.grid, stream);
   if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
   return ok();
 }
@@ -553,12 +628,9 @@ ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   if (ws_bytes < need)
     return fail(MA_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes < %zu",
                 ws_bytes, need);
-  std::shared_ptr<Plan> plan;
-  st = get_plan(1, prob, q_idx, nq, kv_idx, nkv, ch, &plan);
+  PlanView plan;
+  st = upload_plan(1, prob, q_idx, nq, kv_idx, nkv, ch, ws, stream, &plan);
   if (st != MA_OK) return st;
-  hipError_t e = hipMemcpyAsync(ws, plan->host, plan->bytes,
-                                hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
   char* wsb = static_cast<char*>(ws);
   BwdParams bp{};
   bp.q = static_cast<const uint16_t*>(q);
@@ -570,17 +642,17 @@ ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   bp.dq = dq;
   bp.dk = dk;
   bp.dv = dv;
-  bp.delta = reinterpret_cast<float*>(wsb + align_up(plan->bytes));
+  bp.delta = reinterpret_cast<float*>(wsb + align_up(plan.bytes));
   bp.lse2 = reinterpret_cast<float*>(
-      wsb + align_up(plan->bytes) +
+      wsb + align_up(plan.bytes) +
       align_up(static_cast<size_t>(nq) * prob->partition_len *
                prob->num_q_heads * 4));
-  bp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->a.off_ptr);
-  bp.qruns = reinterpret_cast<const DevRun*>(wsb + plan->a.off_runs);
-  bp.qorder = reinterpret_cast<const int2*>(wsb + plan->a.off_order);
-  bp.kvblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan->b.off_ptr);
-  bp.kvruns = reinterpret_cast<const DevRun*>(wsb + plan->b.off_runs);
-  bp.kvorder = reinterpret_cast<const int2*>(wsb + plan->b.off_order);
+  bp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan.a.off_ptr);
+  bp.qruns = reinterpret_cast<const DevRun*>(wsb + plan.a.off_runs);
+  bp.qorder = reinterpret_cast<const int2*>(wsb + plan.a.off_order);
+  bp.kvblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan.b.off_ptr);
+  bp.kvruns = reinterpret_cast<const DevRun*>(wsb + plan.b.off_runs);
+  bp.kvorder = reinterpret_cast<const int2*>(wsb + plan.b.off_order);
   bp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
   bp.rows_kv = int64_t{nkv} * (prob->partition_len / ch.num_kv_chunks);
   bp.hq = prob->num_q_heads;
@@ -589,7 +661,8 @@ ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   bp.scale = prob->softmax_scale;
   bp.scale_log2 = prob->softmax_scale * kLog2e;
   bp.accumulate = accumulate;
-  e = launch_tile_bwd(bp, prob->head_dim, plan->a.grid, plan->b.grid, stream);
+  hipError_t e =
+      launch_tile_bwd(bp, prob->head_dim, plan.a.grid, plan.b.grid, stream);
   if (e != hipSuccess) return hip_fail(e, "tile_bwd launch");
   return ok();
 }
@@ -646,7 +719,7 @@ ma_status_t mesh_attn_classify(const ma_problem_t* prob, const int32_t* q_idx,
 ma_status_t mesh_attn_worklist(const ma_problem_t* prob, const int32_t* q_idx,
                                int32_t nq, const int32_t* kv_idx, int32_t nkv,
                                int32_t bm, int32_t bn, int32_t* qblk_ptr,
-                               int32_t* runs, int64_t cap, int64_t* n_runs) {
+                               ma_run_t* runs, int64_t cap, int64_t* n_runs) {
   ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
   if (st == MA_OK) st = check_blocks(prob, bm, bn);
   if (st != MA_OK) return st;
@@ -662,7 +735,7 @@ ma_status_t mesh_attn_worklist_kv_major(const ma_problem_t* prob,
                                         const int32_t* q_idx, int32_t nq,
                                         const int32_t* kv_idx, int32_t nkv,
                                         int32_t bm, int32_t bn,
-                                        int32_t* kvblk_ptr, int32_t* runs,
+                                        int32_t* kvblk_ptr, ma_run_t* runs,
                                         int64_t cap, int64_t* n_runs) {
   ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
   if (st == MA_OK) st = check_blocks(prob, bm, bn);

@@ -77,7 +77,8 @@ struct BwdParams {
   const int32_t* qblk_ptr;
   const DevRun* qruns;
   const int2* qorder;
-  // KV-major runs (dK/dV kernel): delta field is kv-first minus q-first.
+  // KV-major runs (dK/dV kernel): Q blocks of kBwdBM rows per KV block of
+  // kBwdBN; the delta field is q-first minus kv-first, as in the Q-major runs.
   const int32_t* kvblk_ptr;
   const DevRun* kvruns;
   const int2* kvorder;   // (kvblk, kv head)

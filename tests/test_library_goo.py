@@ -14,6 +14,8 @@ from oracle import goo
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
                       "goo_worked_example.json")
+GOLDEN_NU = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                         "goo_nonuniform.json")
 
 
 def test_worked_example():
@@ -29,6 +31,20 @@ def test_worked_example():
         assert sorted(steps[int(s) - 1][1]) == sorted(map(tuple, tasks))
     assert [n + 1 for n, (cm, _) in enumerate(steps) if cm is None] == \
         g["compute_only_steps"]
+
+
+@pytest.mark.parametrize("case", json.load(open(GOLDEN_NU))["cases"],
+                         ids=lambda c: c["name"])
+def test_nonuniform_golden(case):
+    """Hand-derived schedules with unequal task times: a higher-index chunk
+    that unlocks more compute is chosen (Section 3.4's rule over every
+    schedulable chunk)."""
+    got = ma.mesh_attn_goo_plan(case["k_q"], case["k_kv"], case["t_ag_q"],
+                                case["t_ag_kv"], case["t_rs_q"],
+                                case["t_c"], case["gamma"])
+    want = [((tuple(c) if c else None), [tuple(t) for t in tasks])
+            for c, tasks in case["steps"]]
+    assert got == want
 
 
 @pytest.mark.parametrize("seed", range(40))
@@ -100,7 +116,9 @@ def test_chunk_fwd_rejects_bad_chunks(chunk):
     pointer, so dummy device addresses never reach a kernel."""
     import ctypes
     lib = ma.load_library()
-    prob = ma.Problem(16, 4096, 32, 32, 128, 1, 0.0884, 0)
+    prob = ma.Problem.make(dict(num_partitions=16, partition_len=4096,
+                                num_q_heads=32, num_kv_heads=32, head_dim=128,
+                                causal=1, layout=0, softmax_scale=0.0884))
     q_idx = (ctypes.c_int32 * 1)(4)
     kv_idx = (ctypes.c_int32 * 1)(0)
     ch = ma.Chunk(*chunk)

@@ -205,3 +205,41 @@ def test_product_has_no_cpu_fallback_and_no_oracle_import():
             if f.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text, f
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structs have the header's field offsets and sizes
+    (a C program built from include/mesh_attn.h prints them)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    structs = {"ma_problem_t": ma.Problem, "ma_run_t": ma._binding.Run,
+               "ma_chunk_t": ma.Chunk, "ma_goo_step_t": ma.GooStep}
+    lines = ["#include <stddef.h>", "#include <stdio.h>",
+             '#include "mesh_attn.h"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", '
+                         f'offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([gcc, "-D__HIP_PLATFORM_AMD__", "-I",
+                    os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True,
+                         text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, \
+                (cname, fname)
+    # the problem's field order is the one of the boundary's definition
+    assert [f for f, _ in ma.Problem._fields_] == [
+        "num_partitions", "partition_len", "num_q_heads", "num_kv_heads",
+        "head_dim", "causal", "layout", "softmax_scale"]

@@ -15,6 +15,8 @@ from oracle import goo
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
                       "goo_worked_example.json")
+GOLDEN_NU = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                         "goo_nonuniform.json")
 
 
 def _golden():
@@ -49,6 +51,58 @@ def test_worked_example_schedule():
     assert only == g["compute_only_steps"]
     for n in only:
         assert len(steps[n - 1][1]) == 1
+
+
+def _golden_steps(case):
+    return [((tuple(c) if c else None), [tuple(t) for t in tasks])
+            for c, tasks in case["steps"]]
+
+
+@pytest.mark.parametrize("case", json.load(open(GOLDEN_NU))["cases"],
+                         ids=lambda c: c["name"])
+def test_nonuniform_costs_higher_index_chunk_wins(case):
+    """Hand-derived schedules with unequal task times (Section 3.4's rule
+    over every schedulable chunk): a higher-index AG-Q or AG-KV chunk that
+    unlocks more compute goes before the lowest-index one."""
+    steps = goo.goo_plan(case["k_q"], case["k_kv"], case["t_ag_q"],
+                         case["t_ag_kv"], case["t_rs_q"], case["t_c"],
+                         case["gamma"])
+    assert steps == _golden_steps(case)
+
+
+def test_every_chunk_is_a_candidate():
+    """On random unequal costs the chosen collective always has the highest
+    profit among all schedulable chunks (not only the lowest-index ones)."""
+    rng = np.random.default_rng(77)
+    higher = 0
+    for _ in range(50):
+        kq, kkv = int(rng.integers(2, 5)), int(rng.integers(2, 5))
+        tq, tkv, trs = (float(x) for x in rng.uniform(0.2, 2.0, 3))
+        t_c = rng.uniform(0.1, 2.0, (kq, kkv)).tolist()
+        steps = goo.goo_plan(kq, kkv, tq, tkv, trs, t_c, 1.05)
+        ag_q, ag_kv = set(), set()
+        t_comm = {goo.AG_Q: tq, goo.AG_KV: tkv, goo.RS_Q: trs}
+        for comm, _tasks in steps:
+            if comm is None:
+                continue
+            kind, idx = comm
+            if kind != goo.RS_Q:
+                def unlock(kd, x):
+                    if kd == goo.AG_Q:
+                        return sum(t_c[x][j] for j in sorted(ag_kv))
+                    return sum(t_c[i][x] for i in sorted(ag_q))
+                best = max([unlock(goo.AG_Q, i) / tq for i in range(kq)
+                            if i not in ag_q] +
+                           [unlock(goo.AG_KV, j) / tkv for j in range(kkv)
+                            if j not in ag_kv])
+                assert unlock(kind, idx) / t_comm[kind] >= best - 1e-12
+                pending = ag_q if kind == goo.AG_Q else ag_kv
+                n = kq if kind == goo.AG_Q else kkv
+                if idx != min(x for x in range(n) if x not in pending):
+                    higher += 1
+            (ag_q if kind == goo.AG_Q else ag_kv
+             if kind == goo.AG_KV else set()).add(idx)
+    assert higher > 0
 
 
 def _check_invariants(kq, kkv, tq, tkv, trs, t_c, gamma, steps):
