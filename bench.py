@@ -1,27 +1,36 @@
 #!/usr/bin/env python3
 """Benchmark of the single-GPU tile compute of Mesh-Attention on MI355X.
 
-One step runs every stage of the hot path once, on one stream, with inputs
-resident in HBM:
+One step runs every stage of the hot path, on one stream, with inputs
+resident in HBM (all bf16, head_dim 128):
 
-  fwd    mesh_attn_tile_fwd on the causal 64K-token tile (16 partitions of
-         4096 tokens; Q partitions 4..7 x KV partitions 0..7; 32 heads,
-         head_dim 128, bf16): work list, scores, causal mask, online softmax,
-         PV, epilogue.
-  merge  mesh_attn_lse_merge folding 16 bf16 partials of 4096 rows x 32
-         heads x 128 (the reduce-scatter fold of a 16x16 mesh); two copies of
-         the partials alternate between steps, so the reads come from HBM.
-  bwd    mesh_attn_tile_bwd of the same causal tile (dO from seed 4), using
-         the forward's O and LSE.
+  fwd              mesh_attn_tile_fwd on the headline tile, by default
+                   mesh1m-nc-gqa: one GPU's share of a 1M-token, 256-GPU mesh
+                   (256 partitions of 4096 tokens, Q partitions 16..31 x KV
+                   partitions 32..47, non-causal, 32 query heads on 8 KV
+                   heads) -- the largest single-GPU workload.  Work list,
+                   scores, online softmax, PV, epilogue.
+  fwd_causal64k    the same call on the causal 64K-token tile (16 partitions
+                   of 4096, Q 4..7 x KV 0..7, 32 heads): causal mask, skipped
+                   blocks, diagonal blocks.
+  fwd_mesh1m_causal  the same call on the 1M-token causal tile that straddles
+                   the diagonal (Q 24..39 x KV 16..31, x8 outlier rows).
+  merge            mesh_attn_lse_merge folding 16 bf16 partials of 4096 rows
+                   x 32 heads x 128 (the reduce-scatter fold of a 16x16
+                   mesh); two copies of the partials alternate between steps,
+                   so the reads come from HBM.
+  bwd              mesh_attn_tile_bwd of the causal 64K tile (dO from seed 4)
+                   with that tile's forward O and LSE.
+  chunks           the headline tile's forward as 4x4 GOO chunk tasks
+                   (mesh_attn_chunk_fwd, float32 running partials).
 
-`value` is the forward tile TFLOP/s: algorithmic FLOPs of the tile
+`value` is the headline tile's forward TFLOP/s: algorithmic FLOPs
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
 duration over the timed steps, measured with HIP events on the launch stream.
-`ms_per_step` is the whole step.  Per-stage figures are under `legs` (mean
-and median over the timed steps; the forward's also gives the host time of
-building the tile's work list, which the library caches and which is outside
-the timed steps).
-Prints one JSON line on stdout; progress goes to stderr.
+`roofline` is that kernel against the bf16 dense MFMA peak.  `ms_per_step`
+is the whole step; every stage's figures are under `legs` (mean and median
+over the timed steps).  Prints one JSON line on stdout; progress goes to
+stderr.
 """
 
 import argparse
@@ -37,32 +46,42 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
+ALL_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
+            "chunks")
+LEG_TILE = {"fwd_causal64k": "causal-64k",
+            "fwd_mesh1m_causal": "mesh1m-causal-outlier",
+            "bwd": "bwd-causal-64k"}
+
 
 def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr,
           flush=True)
 
 
-def visible_pairs(cfg):
-    """Number of visible (query, key) pairs of a tile (per head)."""
+def positions(cfg, part_ids):
+    """Global token positions of a stacked partition buffer (contiguous:
+    p * P + r; striped: r * n + p)."""
     import numpy as np
     P = cfg.partition_len
-    total = 0
-    for qp in cfg.q_idx:
-        qpos = qp * P + np.arange(P, dtype=np.int64)
-        for kp in cfg.kv_idx:
-            if not cfg.causal:
-                total += P * P
-            elif cfg.layout == 1:
-                # striped: key row r' visible to query row r iff
-                # r' * n + kp <= r * n + qp, i.e. r' <= r (kp <= qp) or
-                # r' < r (kp > qp)
-                total += P * (P + 1) // 2 - (P if kp > qp else 0)
-            else:
-                k0 = kp * P
-                # keys k0..k0+P-1 visible to query at position x: clamp(x-k0+1)
-                total += int(np.clip(qpos - k0 + 1, 0, P).sum())
-    return total
+    r = np.arange(P, dtype=np.int64)
+    p = np.asarray(part_ids, dtype=np.int64)[:, None]
+    pos = r[None, :] * cfg.num_partitions + p if cfg.layout == 1 \
+        else p * P + r[None, :]
+    return pos.reshape(-1)
+
+
+def visible_pairs(cfg, q_rows=None):
+    """Visible (query, key) pairs of a tile per head, over every query row or
+    over the buffer rows ``q_rows``."""
+    import numpy as np
+    qpos = positions(cfg, cfg.q_idx)
+    if q_rows is not None:
+        qpos = qpos[np.asarray(q_rows)]
+    nk = cfg.nkv * cfg.partition_len
+    if not cfg.causal:
+        return int(qpos.size) * nk
+    kpos = np.sort(positions(cfg, cfg.kv_idx))
+    return int(np.searchsorted(kpos, qpos, side="right").sum())
 
 
 def source_digest(names):
@@ -74,7 +93,7 @@ def source_digest(names):
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel, digest):
+def load_traffic(key, digest):
     """HBM bytes per launch from the committed counter summary, if it was
     taken on the current kernel source (else None)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
@@ -82,29 +101,23 @@ def load_traffic(kernel, digest):
         return None
     with open(path) as f:
         data = json.load(f)
-    ent = data.get(kernel)
+    ent = data.get(key)
     if not ent or ent.get("source_digest") != digest:
         return None
     return ent.get("bytes_per_launch")
 
 
 def cpu_baseline(cfg, budget_s):
-    """Time the float64 oracle on a bounded sample of the forward tile."""
-    import numpy as np
+    """Time the float64 oracle, as it stands, on a bounded sample of the
+    headline tile: sampled query rows, one head after another until the
+    budget is spent, every core of the affinity set for its BLAS."""
     import oracle
     from mesh_inputs import make_qkv, sample_rows
     from threadpoolctl import threadpool_info, threadpool_limits
     cores = len(os.sched_getaffinity(0))
-    cores = min(cores, 16)
     q, k, v, _ = make_qkv(cfg)
     qf, kf, vf = (t.float().numpy() for t in (q, k, v))
-    rows = sample_rows(cfg, cfg.nq, n_random=448)
-    P = cfg.partition_len
-    qpos = np.array([cfg.q_idx[r // P] * P + r % P for r in rows])
-    # visible keys per sampled row (contiguous partitions, causal)
-    kpos = np.concatenate([kp * P + np.arange(P) for kp in cfg.kv_idx])
-    vis = np.array([(kpos <= x).sum() if cfg.causal else kpos.size
-                    for x in qpos])
+    rows = sample_rows(cfg, cfg.nq, n_random=64)
     done_heads = 0
     used = cores
     t0 = time.perf_counter()
@@ -119,7 +132,7 @@ def cpu_baseline(cfg, budget_s):
         if infos:
             used = max(int(i["num_threads"]) for i in infos)
     dt = time.perf_counter() - t0
-    flops = 4.0 * cfg.head_dim * done_heads * float(vis.sum())
+    flops = 4.0 * cfg.head_dim * done_heads * visible_pairs(cfg, rows)
     rate = flops / dt
     cpu_model = "unknown"
     try:
@@ -133,10 +146,55 @@ def cpu_baseline(cfg, budget_s):
     full = 4.0 * cfg.head_dim * cfg.num_q_heads * visible_pairs(cfg)
     return {"value": rate / 1e12, "unit": "TFLOP/s", "cores": used,
             "kind": "oracle", "cpu_model": cpu_model,
+            "affinity_cores": cores,
             "projected_full_tile_s": round(full / rate, 1),
             "sample": (f"float64 oracle forward of {len(rows)} sampled query "
-                       f"rows x {done_heads} heads of the {cfg.name} tile "
-                       f"({flops / 1e9:.1f} GFLOP algorithmic, {dt:.1f} s)")}
+                       f"rows x {done_heads} of {cfg.num_q_heads} heads of "
+                       f"the {cfg.name} tile ({flops / 1e9:.1f} GFLOP "
+                       f"algorithmic, {dt:.1f} s)")}
+
+
+class Tile:
+    """Device buffers of one forward (and optionally backward) workload."""
+
+    def __init__(self, ma, cfg, dev, with_bwd=False, grad_cfg=None):
+        import torch
+        from mesh_inputs import make_grad, make_qkv
+        self.cfg = cfg
+        self.prob = cfg.problem()
+        P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads,
+                         cfg.num_kv_heads, cfg.head_dim)
+        rq, rkv = cfg.nq * P, cfg.nkv * P
+        log(f"generating inputs ({cfg.name})")
+        q, k, v, _ = make_qkv(cfg)
+        self.q, self.k, self.v = (t.to(dev) for t in (q, k, v))
+        del q, k, v
+        self.o = torch.empty((rq, hq, d), dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty((hq, rq), dtype=torch.float32, device=dev)
+        self.ws = torch.empty(ma.mesh_attn_fwd_workspace_size(
+            self.prob, cfg.nq, cfg.nkv), dtype=torch.uint8, device=dev)
+        self.flop = 4.0 * d * hq * visible_pairs(cfg)
+        if with_bwd:
+            self.do = make_grad(grad_cfg or cfg).to(dev)
+            self.dq = torch.empty((rq, hq, d), dtype=torch.float32,
+                                  device=dev)
+            self.dk = torch.empty((rkv, hkv, d), dtype=torch.float32,
+                                  device=dev)
+            self.dv = torch.empty_like(self.dk)
+            self.ws_b = torch.empty(ma.mesh_attn_bwd_workspace_size(
+                self.prob, cfg.nq, cfg.nkv), dtype=torch.uint8, device=dev)
+            self.bwd_flop = 10.0 * d * hq * visible_pairs(cfg)
+
+    def fwd(self, ma):
+        c = self.cfg
+        ma.mesh_attn_tile_fwd(self.prob, c.q_idx, c.kv_idx, self.q, self.k,
+                              self.v, self.o, self.lse, ws=self.ws)
+
+    def bwd(self, ma):
+        c = self.cfg
+        ma.mesh_attn_tile_bwd(self.prob, c.q_idx, c.kv_idx, self.q, self.k,
+                              self.v, self.o, self.do, self.lse, self.dq,
+                              self.dk, self.dv, ws=self.ws_b)
 
 
 def main():
@@ -144,22 +202,17 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--legs", default="fwd,merge,bwd",
-                    help="comma list of fwd, merge, bwd, chunks (chunks: the "
-                         "forward of the same tile as k_Q x k_KV GOO chunk "
-                         "tasks, see --chunks)")
+    ap.add_argument("--legs", default=",".join(ALL_LEGS),
+                    help="comma list of " + ", ".join(ALL_LEGS))
     ap.add_argument("--chunks", default="4x4",
                     help="k_Q x k_KV of the chunks leg")
-    ap.add_argument("--workload", default="causal-64k",
-                    choices=("causal-64k", "mesh1m-nc-gqa",
+    ap.add_argument("--workload", default="mesh1m-nc-gqa",
+                    choices=("mesh1m-nc-gqa", "causal-64k",
                              "mesh1m-causal-outlier", "striped-causal-64k",
                              "striped-mesh1m-causal"),
-                    help="forward tile: causal-64k (default), mesh1m-nc-gqa "
-                         "(1M-token non-causal GQA 16x16 tile), "
-                         "mesh1m-causal-outlier (1M-token causal 16x16 tile "
-                         "with outliers), striped-causal-64k, "
-                         "striped-mesh1m-causal; the backward leg runs on "
-                         "the two 64K tiles only")
+                    help="tile of the headline fwd leg and of the chunks "
+                         "leg (default mesh1m-nc-gqa, the largest "
+                         "single-GPU tile)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -169,61 +222,59 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the library runs on one GPU (asked for "
-              f"--gpus {args.gpus}); the multi-GPU mesh is not implemented.",
+              f"--gpus {args.gpus}); this build has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
     legs = [x for x in args.legs.split(",") if x]
+    for x in legs:
+        if x not in ALL_LEGS:
+            ap.error(f"unknown leg {x}")
 
     import torch
     import paper_2512_20968_amd as ma
-    from mesh_inputs import WORKLOADS, make_grad, make_merge_parts, make_qkv
+    from mesh_inputs import WORKLOADS, make_merge_parts
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg = WORKLOADS[args.workload]
-    if "bwd" in legs and args.workload not in ("causal-64k",
-                                               "striped-causal-64k"):
-        legs.remove("bwd")
-    prob = cfg.problem()
-    P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
-                     cfg.head_dim)
-    rq, rkv = cfg.nq * P, cfg.nkv * P
-    log(f"generating inputs ({cfg.name})")
-    q, k, v, _ = make_qkv(cfg)
-    qd, kd, vd = (t.to(dev) for t in (q, k, v))
-    del q, k, v
-    o = torch.empty((rq, hq, d), dtype=torch.bfloat16, device=dev)
-    lse = torch.empty((hq, rq), dtype=torch.float32, device=dev)
-    ws_f = torch.empty(ma.mesh_attn_fwd_workspace_size(prob, cfg.nq, cfg.nkv),
-                       dtype=torch.uint8, device=dev)
+    head_cfg = WORKLOADS[args.workload]
+    tiles = {}
+    if "fwd" in legs or "chunks" in legs:
+        tiles["fwd"] = Tile(ma, head_cfg, dev)
+    if "fwd_causal64k" in legs:
+        tiles["fwd_causal64k"] = Tile(ma, WORKLOADS["causal-64k"], dev)
+    if "fwd_mesh1m_causal" in legs:
+        tiles["fwd_mesh1m_causal"] = Tile(
+            ma, WORKLOADS["mesh1m-causal-outlier"], dev)
     if "bwd" in legs:
-        # dO of the backward workload of this tile (bwd-causal-64k is the
-        # backward of causal-64k; the striped tile carries its own seed).
-        do = make_grad(WORKLOADS["bwd-causal-64k"]
-                       if args.workload == "causal-64k" else cfg).to(dev)
-        dq = torch.empty((rq, hq, d), dtype=torch.float32, device=dev)
-        dk = torch.empty((rkv, hkv, d), dtype=torch.float32, device=dev)
-        dv = torch.empty_like(dk)
-        ws_b = torch.empty(ma.mesh_attn_bwd_workspace_size(prob, cfg.nq,
-                                                           cfg.nkv),
-                           dtype=torch.uint8, device=dev)
+        # The backward workload is the backward of the causal 64K tile: same
+        # inputs (seed 1), dO from seed 4, O and LSE from its forward, which
+        # runs once here, before timing (the fwd_causal64k leg rewrites the
+        # same values in its own buffers).
+        t = Tile(ma, WORKLOADS["causal-64k"], dev, with_bwd=True,
+                 grad_cfg=WORKLOADS["bwd-causal-64k"])
+        t.fwd(ma)
+        tiles["bwd"] = t
     if "chunks" in legs:
         # The buffers the chunk all-gathers would produce (chunk i of every
         # Q partition, chunk j of every KV partition), built before timing.
+        ht = tiles["fwd"]
+        cfg = head_cfg
+        P, hq, d = cfg.partition_len, cfg.num_q_heads, cfg.head_dim
         kq, kkv = (int(x) for x in args.chunks.lower().split("x"))
         cq, ckv = P // kq, P // kkv
+
         def gather(t, n_parts, c, i):
             return torch.cat([t[a * P + i * c:a * P + (i + 1) * c]
                               for a in range(n_parts)]).contiguous()
-        cqd = [gather(qd, cfg.nq, cq, i) for i in range(kq)]
-        ckd = [gather(kd, cfg.nkv, ckv, j) for j in range(kkv)]
-        cvd = [gather(vd, cfg.nkv, ckv, j) for j in range(kkv)]
+        cqd = [gather(ht.q, cfg.nq, cq, i) for i in range(kq)]
+        ckd = [gather(ht.k, cfg.nkv, ckv, j) for j in range(kkv)]
+        cvd = [gather(ht.v, cfg.nkv, ckv, j) for j in range(kkv)]
         co = [torch.empty((cfg.nq * cq, hq, d), dtype=torch.float32,
                           device=dev) for _ in range(kq)]
         cl = [torch.empty((hq, cfg.nq * cq), dtype=torch.float32, device=dev)
               for _ in range(kq)]
         ws_c = torch.empty(ma.mesh_attn_chunk_fwd_workspace_size(
-            prob, cfg.nq, cfg.nkv), dtype=torch.uint8, device=dev)
+            cfg.problem(), cfg.nq, cfg.nkv), dtype=torch.uint8, device=dev)
     if "merge" in legs:
         mk, mrows, mh, md = 16, 4096, 32, 128
         mo_parts, ml_parts = make_merge_parts(mk, mrows, mh, md, seed=7)
@@ -238,30 +289,32 @@ def main():
     stream = torch.cuda.current_stream()
     step_no = [0]
 
+    def leg(name, ev, fn):
+        if ev:
+            ev[name][0].record(stream)
+        fn()
+        if ev:
+            ev[name][1].record(stream)
+
     def run_step(ev=None):
-        if "fwd" in legs:
-            if ev: ev["fwd"][0].record(stream)
-            ma.mesh_attn_tile_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o,
-                                  lse, ws=ws_f)
-            if ev: ev["fwd"][1].record(stream)
-        if "chunks" in legs:
-            if ev: ev["chunks"][0].record(stream)
-            for i in range(kq):
-                for j in range(kkv):
-                    ma.mesh_attn_chunk_fwd(prob, cfg.q_idx, cfg.kv_idx,
-                                           (i, kq, j, kkv), cqd[i], ckd[j],
-                                           cvd[j], co[i], cl[i],
-                                           accumulate=int(j > 0), ws=ws_c)
-            if ev: ev["chunks"][1].record(stream)
-        if "merge" in legs:
-            if ev: ev["merge"][0].record(stream)
-            ma.mesh_attn_lse_merge(*msets[step_no[0] % 2], mo, ml)
-            if ev: ev["merge"][1].record(stream)
-        if "bwd" in legs:
-            if ev: ev["bwd"][0].record(stream)
-            ma.mesh_attn_tile_bwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o,
-                                  do, lse, dq, dk, dv, ws=ws_b)
-            if ev: ev["bwd"][1].record(stream)
+        for name in legs:
+            if name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
+                leg(name, ev, lambda: tiles[name].fwd(ma))
+            elif name == "bwd":
+                leg(name, ev, lambda: tiles["bwd"].bwd(ma))
+            elif name == "merge":
+                leg(name, ev, lambda: ma.mesh_attn_lse_merge(
+                    *msets[step_no[0] % 2], mo, ml))
+            elif name == "chunks":
+                def chunks():
+                    c = head_cfg
+                    for i in range(kq):
+                        for j in range(kkv):
+                            ma.mesh_attn_chunk_fwd(
+                                c.problem(), c.q_idx, c.kv_idx,
+                                (i, kq, j, kkv), cqd[i], ckd[j], cvd[j],
+                                co[i], cl[i], accumulate=int(j > 0), ws=ws_c)
+                leg(name, ev, chunks)
         step_no[0] += 1
 
     if args.calib_copy:
@@ -297,45 +350,52 @@ def main():
     log(f"step {ms_step:.3f} ms; " +
         ", ".join(f"{n} {leg_ms[n]:.3f} ms" for n in legs))
 
-    # Host time of the canonical work list (built once per tile and cached by
-    # the library, so it is outside the timed steps).
-    bm, bn = ma.mesh_attn_block_shape(d, 0)
-    t_wl = time.perf_counter()
-    _, wl_runs = ma.mesh_attn_worklist(prob, cfg.q_idx, cfg.kv_idx, bm, bn)
-    wl_ms = (time.perf_counter() - t_wl) * 1e3
-
-    pairs = visible_pairs(cfg)
-    fwd_flop = 4.0 * d * hq * pairs
-    bwd_flop = 10.0 * d * hq * pairs
+    fwd_dig = source_digest(["tile_fwd.hip", "tile_common.h", "internal.h"])
     out_legs = {}
     roofline = None
     value = None
-    if "fwd" in legs:
-        tf = fwd_flop / (leg_ms["fwd"] * 1e-3) / 1e12
-        value = tf
-        dig = source_digest(["tile_fwd.hip", "tile_common.h", "internal.h"])
-        roofline = {"bound": "mfma", "achieved": round(tf, 2),
-                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(tf / PEAK_BF16_TFLOPS, 4),
-                    "traffic": load_traffic("tile_fwd", dig),
-                    "kernel": "tile_fwd_kernel<128,bf16 out>",
-                    "flop_per_launch": fwd_flop}
-        out_legs["fwd"] = {"ms": round(leg_ms["fwd"], 4),
-                           "ms_median": round(leg_med["fwd"], 4),
-                           "tflops": round(tf, 2),
-                           "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
-                           "flop": fwd_flop,
-                           "worklist_host_ms": round(wl_ms, 3),
-                           "worklist_runs": int(len(wl_runs))}
+    for name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
+        if name not in legs:
+            continue
+        t = tiles[name]
+        tf = t.flop / (leg_ms[name] * 1e-3) / 1e12
+        # Host time of the tile's canonical work list (built once per tile
+        # and cached by the library, so outside the timed steps).
+        bm, bn = ma.mesh_attn_block_shape(t.cfg.head_dim, 0)
+        t_wl = time.perf_counter()
+        _, wl_runs = ma.mesh_attn_worklist(t.prob, t.cfg.q_idx, t.cfg.kv_idx,
+                                           bm, bn)
+        wl_ms = (time.perf_counter() - t_wl) * 1e3
+        out_legs[name] = {"workload": t.cfg.name,
+                          "ms": round(leg_ms[name], 4),
+                          "ms_median": round(leg_med[name], 4),
+                          "tflops": round(tf, 2),
+                          "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                          "flop": t.flop,
+                          "traffic": load_traffic(f"tile_fwd@{t.cfg.name}",
+                                                  fwd_dig),
+                          "worklist_host_ms": round(wl_ms, 3),
+                          "worklist_runs": int(len(wl_runs))}
+        if name == "fwd":
+            value = tf
+            roofline = {"bound": "mfma", "achieved": round(tf, 2),
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                        "traffic": out_legs[name]["traffic"],
+                        "kernel": "tile_fwd_kernel<128, bf16 out>",
+                        "workload": t.cfg.name,
+                        "flop_per_launch": t.flop}
     if "chunks" in legs:
-        tc = fwd_flop / (leg_ms["chunks"] * 1e-3) / 1e12
-        out_legs["chunks"] = {"ms": round(leg_ms["chunks"], 4),
+        t = tiles["fwd"]
+        tc = t.flop / (leg_ms["chunks"] * 1e-3) / 1e12
+        out_legs["chunks"] = {"workload": t.cfg.name,
+                              "ms": round(leg_ms["chunks"], 4),
                               "ms_median": round(leg_med["chunks"], 4),
                               "tflops": round(tc, 2),
                               "frac_bf16_peak": round(tc / PEAK_BF16_TFLOPS,
                                                       4),
                               "chunks": f"{kq}x{kkv}",
-                              "launches": kq * kkv, "flop": fwd_flop}
+                              "launches": kq * kkv, "flop": t.flop}
     if "merge" in legs:
         mbytes = (mk * mrows * mh * (md * 2 + 4) + mrows * mh * (md * 2 + 4))
         gbs = mbytes / (leg_ms["merge"] * 1e-3) / 1e9
@@ -349,20 +409,28 @@ def main():
                              "shape": f"k={mk} x {mrows} rows x {mh} heads x "
                                       f"{md}, bf16 in/out"}
     if "bwd" in legs:
-        tb = bwd_flop / (leg_ms["bwd"] * 1e-3) / 1e12
-        out_legs["bwd"] = {"ms": round(leg_ms["bwd"], 4),
+        t = tiles["bwd"]
+        tb = t.bwd_flop / (leg_ms["bwd"] * 1e-3) / 1e12
+        out_legs["bwd"] = {"workload": "bwd-causal-64k",
+                           "ms": round(leg_ms["bwd"], 4),
                            "ms_median": round(leg_med["bwd"], 4),
                            "tflops": round(tb, 2),
                            "frac_bf16_peak": round(tb / PEAK_BF16_TFLOPS, 4),
-                           "flop": bwd_flop}
+                           "flop": t.bwd_flop}
 
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on host cores (bounded sample)")
-        cpu = cpu_baseline(cfg, args.cpu_budget)
+        cpu = cpu_baseline(head_cfg, args.cpu_budget)
         log(f"oracle: {cpu['value'] * 1e3:.3f} GFLOP/s on {cpu['cores']} "
             f"threads")
 
+    step_desc = {"fwd": f"tile_fwd({head_cfg.name})",
+                 "fwd_causal64k": "tile_fwd(causal-64k)",
+                 "fwd_mesh1m_causal": "tile_fwd(mesh1m-causal-outlier)",
+                 "merge": "lse_merge(16x4096x32x128)",
+                 "bwd": "tile_bwd(causal-64k)",
+                 "chunks": f"{args.chunks} chunk_fwd({head_cfg.name})"}
     line = {
         "metric": "tile attention fwd TFLOP/s on 1 MI355X + % of bf16 MFMA "
                   "peak; merge GB/s",
@@ -377,14 +445,11 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16 Q/K/V/dO)",
-        "config": {"workload": f"{cfg.name} tile: {cfg.note}; "
-                               f"{hq} q heads / {hkv} kv heads, head_dim {d}"
-                               f"; step = " + " + ".join(
-                                   {"fwd": "tile_fwd", "merge":
-                                    "lse_merge(16x4096x32x128)",
-                                    "bwd": "tile_bwd",
-                                    "chunks": f"{args.chunks} chunk_fwd"}[x]
-                                   for x in legs),
+        "config": {"workload": f"{head_cfg.name} tile: {head_cfg.note}; "
+                               f"{head_cfg.num_q_heads} q heads / "
+                               f"{head_cfg.num_kv_heads} kv heads, head_dim "
+                               f"{head_cfg.head_dim}",
+                   "step": " + ".join(step_desc[x] for x in legs),
                    "legs": legs},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -49,3 +49,17 @@ def test_bench_refuses_more_than_one_gpu():
                         "--gpus", "2"], capture_output=True, text=True,
                        timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_visible_pairs_of_sampled_rows(layout):
+    """The CPU baseline's FLOP count over sampled rows follows the layout
+    (striped positions interleave the partitions)."""
+    cfg = dataclasses.replace(WORKLOADS["causal-64k"], num_partitions=6,
+                              partition_len=16, q_idx=[4, 1, 5],
+                              kv_idx=[0, 5, 2, 1], causal=True, layout=layout)
+    rows = [0, 3, 17, 20, 33, 47]
+    qpos = oracle.problem_positions(cfg.problem(), cfg.q_idx)[rows]
+    kpos = oracle.problem_positions(cfg.problem(), cfg.kv_idx)
+    want = int((kpos[None, :] <= qpos[:, None]).sum())
+    assert bench.visible_pairs(cfg, rows) == want

@@ -12,7 +12,8 @@ import oracle
 import paper_2512_20968_amd as ma
 from mesh_inputs import WORKLOADS, make_grad, make_qkv, sample_rows
 
-from helpers import check_grad, log, run_fwd, to_np
+from helpers import (check_grad, log, oracle_backward_rows, run_fwd,
+                     to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -148,65 +149,90 @@ def test_backward_is_deterministic(gpu):
         assert torch.equal(x, y)
 
 
-def test_causal64k_backward_sampled_rows(gpu):
-    """Full-size backward of the causal 64K tile.  The oracle runs its own
-    float64 forward for every row of three heads, then checks dQ on the
-    sampled Q rows and dK, dV on sampled KV rows of those heads.  On all
-    heads, two identities that hold because the tile holds every key the Q
-    rows can see: sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
-    cfg = WORKLOADS["bwd-causal-64k"]
+def _gpu_backward_cpu(cfg, gpu):
+    """GPU forward and backward of a full-size workload; inputs and gradients
+    returned as CPU tensors (the device copies are freed)."""
     prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
-    log("causal-64k backward: GPU")
+    log(f"{cfg.name}: GPU backward")
     dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     torch.cuda.synchronize()
-    # Identities, all heads.  P and dS are rounded to bf16 before the MFMAs
-    # (relative error 2^-9 per term, random-walking over ~10^4 terms), so the
-    # sums are compared with the L1 mass of the terms they add up.
-    sdk = dk.sum(0)
-    sdv = dv.sum(0)
-    sdo = dod.float().sum(0)
-    mass_k = dk.abs().sum(0)
-    mass_v = dv.abs().sum(0)
-    rk = float((sdk.abs() / mass_k).max())
-    rv = float(((sdv - sdo).abs() / mass_v).max())
+    out = dict(prob=prob, q=q, k=k, v=v, do=do, dq=dq.cpu(), dk=dk.cpu(),
+               dv=dv.cpu())
+    del qd, kd, vd, dod, o, lse, dq, dk, dv
+    torch.cuda.empty_cache()
+    return out
+
+
+@pytest.fixture(scope="module")
+def bwd64k(gpu):
+    return _gpu_backward_cpu(WORKLOADS["bwd-causal-64k"], gpu)
+
+
+@pytest.fixture(scope="module")
+def bwd1m(gpu):
+    return _gpu_backward_cpu(
+        dataclasses.replace(WORKLOADS["mesh1m-nc-gqa"], grad_seed=8), gpu)
+
+
+def test_causal64k_backward_identities(bwd64k):
+    """Full-size backward of the causal 64K tile, all heads: the tile holds
+    every key its Q rows can see, so sum_j dK_j = 0 and sum_j dV_j = sum_i
+    dO_i.  P and dS are rounded to bf16 before the MFMAs (relative error 2^-9
+    per term, random-walking over ~10^4 terms), so the sums are compared with
+    the L1 mass of the terms they add up."""
+    dk, dv, do = bwd64k["dk"], bwd64k["dv"], bwd64k["do"]
+    rk = float((dk.sum(0).abs() / dk.abs().sum(0)).max())
+    rv = float(((dv.sum(0) - do.float().sum(0)).abs() / dv.abs().sum(0)).max())
     log(f"causal-64k backward: max |sum dK| / sum|dK| = {rk:.3e}, "
         f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
     assert rk <= 1e-2 and rv <= 1e-2
-    heads = [0, 17, 31]
+
+
+@pytest.mark.parametrize("heads", [range(0, 16), range(16, 32)],
+                         ids=["heads0-15", "heads16-31"])
+def test_causal64k_backward_sampled_rows(bwd64k, heads):
+    """Full-size backward of the causal 64K tile against the float64 oracle,
+    on every head (half of them per test): dQ on the sampled Q rows and dK,
+    dV on the sampled KV rows.  The oracle's forward covers every row of
+    each head (its LSE and D enter every dK, dV row)."""
+    cfg = WORKLOADS["bwd-causal-64k"]
+    b = bwd64k
+    heads = list(heads)
     q_rows = sample_rows(cfg, cfg.nq)
     kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000)
-    log(f"causal-64k backward: oracle on heads {heads}, {len(q_rows)} dQ rows, "
-        f"{len(kv_rows)} dK/dV rows")
-    rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
-        prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do),
-        kv_heads=heads, q_rows=q_rows, kv_rows=kv_rows)
-    qr = torch.tensor(q_rows, device=gpu)
-    kr = torch.tensor(kv_rows, device=gpu)
-    check_grad("causal-64k dq", to_np(dq[qr][:, q_heads]), rdq)
-    check_grad("causal-64k dk", to_np(dk[kr][:, heads]), rdk)
-    check_grad("causal-64k dv", to_np(dv[kr][:, heads]), rdv)
+    log(f"causal-64k backward: oracle on heads {heads[0]}..{heads[-1]}, "
+        f"{len(q_rows)} dQ rows, {len(kv_rows)} dK/dV rows")
+    rdq, rdk, rdv, q_heads = oracle_backward_rows(
+        b["prob"], cfg.q_idx, cfg.kv_idx, b["q"], b["k"], b["v"], b["do"],
+        heads, q_rows, kv_rows)
+    assert q_heads == heads
+    for i, h in enumerate(heads):
+        check_grad(f"causal-64k dq h{h}", to_np(b["dq"][q_rows][:, h]),
+                   rdq[:, i])
+        check_grad(f"causal-64k dk h{h}", to_np(b["dk"][kv_rows][:, h]),
+                   rdk[:, i])
+        check_grad(f"causal-64k dv h{h}", to_np(b["dv"][kv_rows][:, h]),
+                   rdv[:, i])
 
 
-def test_mesh1m_gqa_backward_full_size(gpu):
+def test_mesh1m_gqa_backward_identities_and_dq(bwd1m):
     """Backward at the 1M-token non-causal GQA tile's full size (65536 rows,
-    32 query heads on 8 KV heads).  dQ of sampled rows of two query heads (in
-    different KV groups) against the float64 definition on those rows; on
-    every KV head, the identities that hold because each row's softmax runs
-    over exactly the tile's keys: sum_j dK_j = 0 and sum_j dV_j = sum of dO
-    over the rows and the query heads of the group."""
+    32 query heads on 8 KV heads).  On every KV head, the identities that
+    hold because each row's softmax runs over exactly the tile's keys: sum_j
+    dK_j = 0 and sum_j dV_j = sum of dO over the rows and the query heads of
+    the group.  dQ of sampled rows of two query heads (in different KV
+    groups) against the float64 definition on those rows."""
     from oracle.attention import (attention_rows, attention_rows_bwd,
                                   problem_positions)
     cfg = dataclasses.replace(WORKLOADS["mesh1m-nc-gqa"], grad_seed=8)
-    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
-    log("mesh1m-nc-gqa backward: GPU")
-    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse)
-    torch.cuda.synchronize()
+    b = bwd1m
+    prob = b["prob"]
+    q, k, v, do, dq, dk, dv = (b[x] for x in
+                               ("q", "k", "v", "do", "dq", "dk", "dv"))
     g = cfg.num_q_heads // cfg.num_kv_heads
-    sdk = dk.sum(0)
-    sdv = dv.sum(0)
-    sdo = dod.float().sum(0).view(cfg.num_kv_heads, g, -1).sum(1)
-    rk = float((sdk.abs() / dk.abs().sum(0)).max())
-    rv = float(((sdv - sdo).abs() / dv.abs().sum(0)).max())
+    sdo = do.float().sum(0).view(cfg.num_kv_heads, g, -1).sum(1)
+    rk = float((dk.sum(0).abs() / dk.abs().sum(0)).max())
+    rv = float(((dv.sum(0) - sdo).abs() / dv.abs().sum(0)).max())
     log(f"mesh1m-nc-gqa backward: max |sum dK| / sum|dK| = {rk:.3e}, "
         f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
     assert rk <= 1e-2 and rv <= 1e-2
@@ -223,5 +249,29 @@ def test_mesh1m_gqa_backward_full_size(gpu):
         D = np.sum(doh * oh, axis=1)
         rdq, _, _ = attention_rows_bwd(qh, kh, vh, doh, lh, D, qpos[rows],
                                        kpos, False, scale)
-        got = to_np(dq[torch.as_tensor(rows, device=gpu), h])
-        check_grad(f"mesh1m-nc-gqa dq head {h} ({len(rows)} rows)", got, rdq)
+        check_grad(f"mesh1m-nc-gqa dq head {h} ({len(rows)} rows)",
+                   to_np(dq[rows, h]), rdq)
+
+
+@pytest.mark.parametrize("kv_head", [0, 7])
+def test_mesh1m_gqa_backward_dkdv_sampled(bwd1m, kv_head):
+    """dK and dV of one KV head at the 1M-token GQA tile's full size, element
+    by element on sampled KV rows, summed over the group's four query heads,
+    against the float64 oracle (whose forward covers all 65536 rows of each
+    of those heads); dQ of those heads on sampled rows as well."""
+    cfg = dataclasses.replace(WORKLOADS["mesh1m-nc-gqa"], grad_seed=8)
+    b = bwd1m
+    q_rows = sample_rows(cfg, cfg.nq, n_random=4)
+    kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000, n_random=16)
+    log(f"mesh1m-nc-gqa backward: oracle on KV head {kv_head}, "
+        f"{len(kv_rows)} dK/dV rows, {len(q_rows)} dQ rows")
+    rdq, rdk, rdv, q_heads = oracle_backward_rows(
+        b["prob"], cfg.q_idx, cfg.kv_idx, b["q"], b["k"], b["v"], b["do"],
+        [kv_head], q_rows, kv_rows)
+    check_grad(f"mesh1m-nc-gqa dk kv head {kv_head}",
+               to_np(b["dk"][kv_rows][:, kv_head]), rdk[:, 0])
+    check_grad(f"mesh1m-nc-gqa dv kv head {kv_head}",
+               to_np(b["dv"][kv_rows][:, kv_head]), rdv[:, 0])
+    for i, h in enumerate(q_heads):
+        check_grad(f"mesh1m-nc-gqa dq head {h}", to_np(b["dq"][q_rows][:, h]),
+                   rdq[:, i])

@@ -1,9 +1,11 @@
-"""Every row and head of the large tiles against the float64 oracle (the
-sampled-row tests cover them by default).  Opt-in: the oracle's full forward
-takes minutes of host time (causal 64K: 8.8 TFLOP in float64, ~75 s on 16
-cores; the 1M-token tiles about eight times that), so it runs only with
-MESH_ATTN_FULL_TILE set to a comma list of workload names (e.g.
-"causal-64k" or "causal-64k,mesh1m-nc-gqa,mesh1m-causal-outlier")."""
+"""Every row and head of the large forward tiles against the float64 oracle.
+
+The causal 64K tile (16384 rows x 32 heads, 8.8 TFLOP of float64 oracle
+work) runs by default: the oracle's row function is spread over the host
+cores, one (head, row chunk) per worker task, which takes well under a
+minute on 16 cores.  The 1M-token tiles need about eight times that work and
+run only when MESH_ATTN_FULL_TILE names them (a comma list, e.g.
+"mesh1m-nc-gqa,mesh1m-causal-outlier")."""
 
 import os
 import time
@@ -12,41 +14,41 @@ import numpy as np
 import pytest
 import torch
 
-import oracle
 from mesh_inputs import WORKLOADS, make_qkv
 
-from helpers import check_fwd, log, run_fwd, to_np
+from helpers import check_fwd, log, oracle_forward_rows, run_fwd, to_np
 
-pytestmark = [
-    pytest.mark.gpu,
-    pytest.mark.skipif(not os.environ.get("MESH_ATTN_FULL_TILE"),
-                       reason="full-tile oracle run is opt-in "
-                              "(MESH_ATTN_FULL_TILE=<workload names>)"),
-]
+pytestmark = pytest.mark.gpu
+
+OPT_IN = ("mesh1m-nc-gqa", "mesh1m-causal-outlier")
 
 
-@pytest.mark.parametrize(
-    "name", ["causal-64k", "mesh1m-nc-gqa", "mesh1m-causal-outlier"])
+@pytest.mark.parametrize("name", ["causal-64k", *OPT_IN])
 def test_every_row_every_head(gpu, name):
-    wanted = os.environ.get("MESH_ATTN_FULL_TILE", "").split(",")
-    if name not in wanted:
-        pytest.skip(f"workload {name} not selected")
+    if name in OPT_IN and name not in os.environ.get(
+            "MESH_ATTN_FULL_TILE", "").split(","):
+        pytest.skip(f"{name}: full-tile oracle run is opt-in "
+                    "(MESH_ATTN_FULL_TILE=<workload names>)")
     cfg = WORKLOADS[name]
     q, k, v, _ = make_qkv(cfg)
     qd, kd, vd = (t.to(gpu) for t in (q, k, v))
     o, lse = run_fwd(cfg.problem(), cfg.q_idx, cfg.kv_idx, qd, kd, vd)
     torch.cuda.synchronize()
     og, lg = to_np(o), to_np(lse)
-    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    del qd, kd, vd, o, lse
+    rows = np.arange(cfg.nq * cfg.partition_len)
     worst_o = worst_l = 0.0
     t0 = time.time()
-    for h in range(cfg.num_q_heads):
-        ro, rl = oracle.tile_forward(cfg.problem(), cfg.q_idx, cfg.kv_idx, qn,
-                                     kn, vn, heads=[h])
-        eo, el = check_fwd(f"{name} head {h} (all {ro.shape[0]} rows)",
-                           og[:, h:h + 1], lg[h:h + 1], ro, rl)
+    # Eight heads per oracle batch keeps the float64 results of a batch at a
+    # few GB.
+    for h0 in range(0, cfg.num_q_heads, 8):
+        heads = list(range(h0, min(cfg.num_q_heads, h0 + 8)))
+        ro, rl = oracle_forward_rows(cfg.problem(), cfg.q_idx, cfg.kv_idx, q,
+                                     k, v, rows, heads)
+        eo, el = check_fwd(f"{name} heads {heads[0]}..{heads[-1]} "
+                           f"(all {rows.size} rows)", og[:, heads],
+                           lg[heads], ro, rl)
         worst_o, worst_l = max(worst_o, eo), max(worst_l, el)
-        log(f"  head {h} done, {time.time() - t0:.0f} s")
+        log(f"  heads {heads[0]}..{heads[-1]} done, {time.time() - t0:.0f} s")
     log(f"{name}, every row and head: max|O err| {worst_o:.3e}, "
         f"max|LSE err| {worst_l:.3e}")
-    assert np.isfinite(worst_o) and np.isfinite(worst_l)

@@ -14,7 +14,8 @@ import oracle
 import paper_2512_20968_amd as ma
 from mesh_inputs import WORKLOADS, make_grad, make_qkv, sample_rows
 
-from helpers import check_fwd, check_grad, log, run_fwd, to_np
+from helpers import (check_fwd, check_grad, log, oracle_backward_rows,
+                     oracle_forward_rows, run_fwd, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -83,11 +84,10 @@ def test_striped_workloads_sampled(gpu, name):
     o, lse = run_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd)
     torch.cuda.synchronize()
     rows = sample_rows(cfg, cfg.nq)
-    heads = (list(range(cfg.num_q_heads)) if name == "striped-causal-64k"
-             else [0, 13, 31])
+    heads = list(range(cfg.num_q_heads))
     log(f"{cfg.name}: oracle on {len(rows)} rows x {len(heads)} heads")
-    ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, to_np(q),
-                                 to_np(k), to_np(v), rows=rows, heads=heads)
+    ro, rl = oracle_forward_rows(prob, cfg.q_idx, cfg.kv_idx, q, k, v, rows,
+                                 heads)
     r = torch.tensor(rows, device=gpu)
     check_fwd(f"{cfg.name} sampled", to_np(o[r][:, heads]),
               to_np(lse[heads][:, r]), ro, rl)
@@ -128,8 +128,9 @@ def test_striped_backward_every_row(gpu, q_idx, kv_idx, d, hq, hkv):
 
 
 def test_striped_causal64k_backward_sampled(gpu):
-    """Full-size backward of the striped 64K tile; the oracle checks two
-    heads on sampled rows (its forward covers every row of those heads)."""
+    """Full-size backward of the striped 64K tile against the float64
+    oracle on every head: dQ on sampled Q rows, dK and dV on sampled KV rows
+    (the oracle's forward covers every row of each head)."""
     cfg = WORKLOADS["striped-causal-64k"]
     prob = cfg.problem()
     (q, k, v), (qd, kd, vd) = _inputs(cfg, gpu)
@@ -139,14 +140,13 @@ def test_striped_causal64k_backward_sampled(gpu):
     log("striped-causal-64k: GPU backward")
     dq, dk, dv = _bwd(prob, cfg, qd, kd, vd, o, dod, lse)
     torch.cuda.synchronize()
-    heads = [3, 30]
+    heads = list(range(cfg.num_q_heads))
     q_rows = sample_rows(cfg, cfg.nq, n_random=16)
     kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000, n_random=16)
-    log(f"striped-causal-64k: oracle on heads {heads}, {len(q_rows)} dQ rows, "
-        f"{len(kv_rows)} dK/dV rows")
-    rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(
-        prob, cfg.q_idx, cfg.kv_idx, to_np(q), to_np(k), to_np(v), to_np(do),
-        kv_heads=heads, q_rows=q_rows, kv_rows=kv_rows)
+    log(f"striped-causal-64k: oracle on {len(heads)} heads, {len(q_rows)} dQ "
+        f"rows, {len(kv_rows)} dK/dV rows")
+    rdq, rdk, rdv, q_heads = oracle_backward_rows(
+        prob, cfg.q_idx, cfg.kv_idx, q, k, v, do, heads, q_rows, kv_rows)
     qr = torch.tensor(q_rows, device=gpu)
     kr = torch.tensor(kv_rows, device=gpu)
     check_grad("striped-causal-64k dq", to_np(dq[qr][:, q_heads]), rdq)
