@@ -168,6 +168,37 @@ ma_status_t mesh_attn_tile_fwd(const ma_problem_t* prob, const int32_t* q_idx,
                                void* o, ma_dtype_t o_dtype, float* lse,
                                void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Maximum size of the scratch array of mesh_attn_tile_fwd_noalloc, per GPU. */
+#define MA_NOALLOC_SCRATCH_BYTES (8u << 20)
+/* Longest index list, and most forward Q blocks (nq * P / 256), it serves. */
+#define MA_NOALLOC_MAX_LIST 256
+#define MA_NOALLOC_MAX_QBLOCKS 4096
+
+/* mesh_attn_tile_fwd for callers that cannot allocate memory: code under
+ * stream (graph) capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments and results as mesh_attn_tile_fwd without the
+ * workspace: the work list is built on the device (from the index lists,
+ * passed by value as kernel arguments) into a scratch array of
+ * MA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends.  The call allocates nothing (no hipMalloc, no
+ * pinned host memory, no host heap), copies nothing from the host and never
+ * synchronizes.
+ * Limits: nq, nkv <= MA_NOALLOC_MAX_LIST; nq * P / 256 <= MA_NOALLOC_MAX_QBLOCKS;
+ * the tile's work list (mesh_attn_fwd_workspace_size bytes) must fit the
+ * scratch array.  Larger tiles return MA_ERR_UNSUPPORTED with the sizes in
+ * mesh_attn_last_error(), before anything is launched.
+ * Every call on one GPU shares that GPU's scratch array (each call rewrites
+ * it before reading it): calls on one stream are ordered, but calls that
+ * overlap on one GPU (different streams without ordering between them) race
+ * and give undefined results. */
+ma_status_t mesh_attn_tile_fwd_noalloc(const ma_problem_t* prob,
+                                       const int32_t* q_idx, int32_t nq,
+                                       const int32_t* kv_idx, int32_t nkv,
+                                       const void* q, const void* k,
+                                       const void* v, void* o,
+                                       ma_dtype_t o_dtype, float* lse,
+                                       hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Greedy Overlapping Optimization (GOO, Section 3.4): chunk compute tasks and
  * the step planner.  Each Q partition of the tile is cut into k_Q chunks of

@@ -15,6 +15,7 @@ from ._binding import (  # noqa: F401
     MA_CLS_FULL,
     MeshAttnError,
     Problem,
+    Run,
     library_path,
     load_library,
     exported_symbols,
@@ -25,6 +26,7 @@ from ._binding import (  # noqa: F401
     mesh_attn_fwd_workspace_size,
     mesh_attn_bwd_workspace_size,
     mesh_attn_tile_fwd,
+    mesh_attn_tile_fwd_noalloc,
     mesh_attn_lse_merge,
     mesh_attn_tile_bwd,
     mesh_attn_chunk_fwd_workspace_size,

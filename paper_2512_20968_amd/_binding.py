@@ -111,6 +111,8 @@ _SIGNATURES = {
     "mesh_attn_bwd_workspace_size": (_sz, [_PROB, _i32, _i32]),
     "mesh_attn_tile_fwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _p, _p, _p,
                                   _p, _i32, _p, _p, _sz, _p]),
+    "mesh_attn_tile_fwd_noalloc": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _p,
+                                          _p, _p, _p, _i32, _p, _p]),
     "mesh_attn_lse_merge": (_i32, [_i32, _i64, _i32, _i32, _p, _i32, _p, _p,
                                    _i32, _p, _p]),
     "mesh_attn_tile_bwd": (_i32, [_PROB, _I32P, _i32, _I32P, _i32, _p, _p, _p,
@@ -315,6 +317,31 @@ def mesh_attn_tile_fwd(prob, q_idx, kv_idx, q, k, v, o, lse, ws=None,
         ctypes.byref(pr), qp, nq, kp, nkv, *args[:3], args[3], _dtype_code(o),
         lp, ctypes.c_void_p(ws.data_ptr()), wsb, _stream_ptr(stream))
     _check("mesh_attn_tile_fwd", st)
+    return o, lse
+
+
+def mesh_attn_tile_fwd_noalloc(prob, q_idx, kv_idx, q, k, v, o, lse,
+                               stream=None):
+    """``mesh_attn_tile_fwd`` without a workspace: the library builds the work
+    list on the device in its own fixed scratch array and allocates
+    nothing."""
+    torch = _torch()
+    pr = Problem.make(prob)
+    qa, qp, nq = _idx(q_idx)
+    ka, kp, nkv = _idx(kv_idx)
+    P, hq, hkv, d = (pr.partition_len, pr.num_q_heads, pr.num_kv_heads,
+                     pr.head_dim)
+    args = [
+        _dev(q, "q", (nq * P, hq, d), (torch.bfloat16,)),
+        _dev(k, "k", (nkv * P, hkv, d), (torch.bfloat16,)),
+        _dev(v, "v", (nkv * P, hkv, d), (torch.bfloat16,)),
+        _dev(o, "o", (nq * P, hq, d), (torch.bfloat16, torch.float32)),
+    ]
+    lp = _dev(lse, "lse", (hq, nq * P), (torch.float32,))
+    st = load_library().mesh_attn_tile_fwd_noalloc(
+        ctypes.byref(pr), qp, nq, kp, nkv, *args[:3], args[3], _dtype_code(o),
+        lp, _stream_ptr(stream))
+    _check("mesh_attn_tile_fwd_noalloc", st)
     return o, lse
 
 

@@ -25,6 +25,11 @@
 
 using namespace mesh_attn;
 
+static_assert(MA_NOALLOC_SCRATCH_BYTES == kNoAllocScratchBytes &&
+                  MA_NOALLOC_MAX_LIST == kNoAllocMaxList &&
+                  MA_NOALLOC_MAX_QBLOCKS == kNoAllocMaxQBlocks,
+              "public limits of the allocation-free forward");
+
 namespace {
 thread_local std::string g_last_error;
 }  // namespace
@@ -789,6 +794,94 @@ ma_status_t mesh_attn_chunk_fwd(const ma_problem_t* prob, const int32_t* q_idx,
                 accumulate);
   return fwd_impl(prob, q_idx, nq, kv_idx, nkv, *chunk, q, k, v, o, true, lse,
                   accumulate, ws, ws_bytes, stream);
+}
+
+ma_status_t mesh_attn_tile_fwd_noalloc(const ma_problem_t* prob,
+                                       const int32_t* q_idx, int32_t nq,
+                                       const int32_t* kv_idx, int32_t nkv,
+                                       const void* q, const void* k,
+                                       const void* v, void* o,
+                                       ma_dtype_t o_dtype, float* lse,
+                                       hipStream_t stream) {
+  if (o_dtype != MA_BF16 && o_dtype != MA_FP32)
+    return fail(MA_ERR_INVALID_ARG, "o_dtype %d invalid", (int)o_dtype);
+  ma_status_t st = check_tile(prob, q_idx, nq, kv_idx, nkv);
+  if (st == MA_OK) st = check_head_dim(prob);
+  if (st == MA_OK) st = check_blocks(prob, kFwdBM, kFwdBN);
+  if (st != MA_OK) return st;
+  const void* ptrs[] = {q, k, v, o, lse};
+  const char* names[] = {"q", "k", "v", "o", "lse"};
+  for (int i = 0; i < 5; ++i) {
+    if (!ptrs[i]) return fail(MA_ERR_INVALID_ARG, "%s is NULL", names[i]);
+    if (!aligned16(ptrs[i]))
+      return fail(MA_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  }
+  if (nq > kNoAllocMaxList || nkv > kNoAllocMaxList)
+    return fail(MA_ERR_UNSUPPORTED,
+                "noalloc forward: index lists of %d and %d partitions exceed "
+                "the maximum of %d", nq, nkv, kNoAllocMaxList);
+  const int64_t nqb = int64_t{nq} * prob->partition_len / kFwdBM;
+  const size_t need = fwd_ws_bound(prob, nq, nkv);
+  if (nqb > kNoAllocMaxQBlocks || need > kNoAllocScratchBytes)
+    return fail(MA_ERR_UNSUPPORTED,
+                "noalloc forward: the tile's work list (%lld Q blocks, %zu "
+                "bytes) exceeds the scratch maximum (%d Q blocks, %zu bytes)",
+                static_cast<long long>(nqb), need, kNoAllocMaxQBlocks,
+                kNoAllocScratchBytes);
+  void* scratch = nullptr;
+  hipError_t e = noalloc_scratch(&scratch);
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  // Same regions as the uploaded plan: Q-block pointers, runs, order.
+  char* base = static_cast<char*>(scratch);
+  const size_t off_runs = align_up(static_cast<size_t>(nqb + 1) * 4);
+  const size_t off_order =
+      off_runs + align_up(static_cast<size_t>(nqb) * nkv * 2 * sizeof(DevRun));
+  const int64_t items = nqb * prob->num_q_heads;
+  const bool by_kv = prob->num_kv_heads % kNumXcd == 0;
+  const int64_t grid = by_kv ? items : (items + kNumXcd - 1) / kNumXcd * kNumXcd;
+  if (grid > INT32_MAX)
+    return fail(MA_ERR_UNSUPPORTED, "noalloc forward: %lld workgroups",
+                static_cast<long long>(grid));
+  PlanBuildParams bp{};
+  bp.P = prob->partition_len;
+  bp.n = prob->num_partitions;
+  bp.layout = prob->layout;
+  bp.causal = prob->causal;
+  bp.nq = nq;
+  bp.nkv = nkv;
+  bp.hq = prob->num_q_heads;
+  bp.hkv = prob->num_kv_heads;
+  bp.group = prob->num_q_heads / prob->num_kv_heads;
+  bp.bm = kFwdBM;
+  bp.bn = kFwdBN;
+  bp.nqb = static_cast<int32_t>(nqb);
+  bp.nkbp = prob->partition_len / kFwdBN;
+  bp.grid = static_cast<int32_t>(grid);
+  bp.qblk_ptr = reinterpret_cast<int32_t*>(base);
+  bp.runs = reinterpret_cast<DevRun*>(base + off_runs);
+  bp.order = reinterpret_cast<int2*>(base + off_order);
+  for (int32_t i = 0; i < nq; ++i) bp.q_idx[i] = q_idx[i];
+  for (int32_t i = 0; i < nkv; ++i) bp.kv_idx[i] = kv_idx[i];
+  e = launch_fwd_plan_build(bp, stream);
+  if (e != hipSuccess) return hip_fail(e, "noalloc work-list build launch");
+  FwdParams fp{};
+  fp.q = static_cast<const uint16_t*>(q);
+  fp.k = static_cast<const uint16_t*>(k);
+  fp.v = static_cast<const uint16_t*>(v);
+  fp.o = o;
+  fp.lse = lse;
+  fp.qblk_ptr = bp.qblk_ptr;
+  fp.runs = bp.runs;
+  fp.order = bp.order;
+  fp.rows_q = int64_t{nq} * prob->partition_len;
+  fp.hq = prob->num_q_heads;
+  fp.hkv = prob->num_kv_heads;
+  fp.group = bp.group;
+  fp.scale_log2 = prob->softmax_scale * kLog2e;
+  fp.accumulate = 0;
+  e = launch_tile_fwd(fp, prob->head_dim, o_dtype == MA_FP32, bp.grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
+  return ok();
 }
 
 ma_status_t mesh_attn_lse_merge(int32_t k_parts, int64_t rows, int32_t heads,

@@ -91,6 +91,35 @@ struct BwdParams {
 hipError_t launch_tile_bwd(const BwdParams& p, int head_dim, int grid_q,
                            int grid_kv, hipStream_t stream);
 
+// ---------------------------------------------------------------------------
+// Allocation-free forward (noalloc.hip): the work list is built on the device
+// into a fixed scratch array instead of a caller workspace.
+// ---------------------------------------------------------------------------
+
+constexpr size_t kNoAllocScratchBytes = size_t{8} << 20;  // per GPU
+constexpr int kNoAllocMaxList = 256;      // partitions per index list
+constexpr int kNoAllocMaxQBlocks = 4096;  // forward Q blocks of the tile
+
+struct PlanBuildParams {
+  int32_t P, n, layout, causal;   // problem (partition length, partitions)
+  int32_t nq, nkv, hq, hkv, group;
+  int32_t bm, bn;                 // forward block shape
+  int32_t nqb, nkbp;              // Q blocks of the tile, KV blocks per part
+  int32_t grid;                   // workgroup slots of the order
+  int32_t* qblk_ptr;              // [nqb + 1] in the scratch array
+  DevRun* runs;                   // [<= 2 nqb nkv]
+  int2* order;                    // [grid]
+  int32_t q_idx[kNoAllocMaxList];
+  int32_t kv_idx[kNoAllocMaxList];
+};
+
+// Device address of the scratch array on the current device (looked up with
+// hipGetSymbolAddress on the first call per device, then cached).
+hipError_t noalloc_scratch(void** ptr);
+
+// Builds the forward work list and workgroup order of `p` (one workgroup).
+hipError_t launch_fwd_plan_build(const PlanBuildParams& p, hipStream_t stream);
+
 // Kernels with more than 64 KB of dynamic LDS need the limit raised once per
 // kernel and device; this does it on the first launch on each device (ids
 // below 64; higher ids set it on every launch).  Safe to call from several
