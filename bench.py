@@ -23,6 +23,8 @@ resident in HBM (all bf16, head_dim 128):
                    with that tile's forward O and LSE.
   chunks           the headline tile's forward as 4x4 GOO chunk tasks
                    (mesh_attn_chunk_fwd, float32 running partials).
+  bwd_striped      (not in the default step) the backward of the striped
+                   64K tile (dO from seed 6).
 
 `value` is the headline tile's forward TFLOP/s: algorithmic FLOPs
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
@@ -46,11 +48,9 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
-ALL_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
-            "chunks")
-LEG_TILE = {"fwd_causal64k": "causal-64k",
-            "fwd_mesh1m_causal": "mesh1m-causal-outlier",
-            "bwd": "bwd-causal-64k"}
+DEFAULT_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
+                "chunks")
+ALL_LEGS = DEFAULT_LEGS + ("bwd_striped",)
 
 
 def log(msg):
@@ -202,7 +202,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--legs", default=",".join(ALL_LEGS),
+    ap.add_argument("--legs", default=",".join(DEFAULT_LEGS),
                     help="comma list of " + ", ".join(ALL_LEGS))
     ap.add_argument("--chunks", default="4x4",
                     help="k_Q x k_KV of the chunks leg")
@@ -254,6 +254,10 @@ def main():
                  grad_cfg=WORKLOADS["bwd-causal-64k"])
         t.fwd(ma)
         tiles["bwd"] = t
+    if "bwd_striped" in legs:
+        t = Tile(ma, WORKLOADS["striped-causal-64k"], dev, with_bwd=True)
+        t.fwd(ma)
+        tiles["bwd_striped"] = t
     if "chunks" in legs:
         # The buffers the chunk all-gathers would produce (chunk i of every
         # Q partition, chunk j of every KV partition), built before timing.
@@ -300,8 +304,8 @@ def main():
         for name in legs:
             if name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
                 leg(name, ev, lambda: tiles[name].fwd(ma))
-            elif name == "bwd":
-                leg(name, ev, lambda: tiles["bwd"].bwd(ma))
+            elif name in ("bwd", "bwd_striped"):
+                leg(name, ev, lambda: tiles[name].bwd(ma))
             elif name == "merge":
                 leg(name, ev, lambda: ma.mesh_attn_lse_merge(
                     *msets[step_no[0] % 2], mo, ml))
@@ -408,15 +412,18 @@ def main():
                              "bytes": mbytes,
                              "shape": f"k={mk} x {mrows} rows x {mh} heads x "
                                       f"{md}, bf16 in/out"}
-    if "bwd" in legs:
-        t = tiles["bwd"]
-        tb = t.bwd_flop / (leg_ms["bwd"] * 1e-3) / 1e12
-        out_legs["bwd"] = {"workload": "bwd-causal-64k",
-                           "ms": round(leg_ms["bwd"], 4),
-                           "ms_median": round(leg_med["bwd"], 4),
-                           "tflops": round(tb, 2),
-                           "frac_bf16_peak": round(tb / PEAK_BF16_TFLOPS, 4),
-                           "flop": t.bwd_flop}
+    for name in ("bwd", "bwd_striped"):
+        if name not in legs:
+            continue
+        t = tiles[name]
+        tb = t.bwd_flop / (leg_ms[name] * 1e-3) / 1e12
+        out_legs[name] = {"workload": ("bwd-causal-64k" if name == "bwd"
+                                       else t.cfg.name),
+                          "ms": round(leg_ms[name], 4),
+                          "ms_median": round(leg_med[name], 4),
+                          "tflops": round(tb, 2),
+                          "frac_bf16_peak": round(tb / PEAK_BF16_TFLOPS, 4),
+                          "flop": t.bwd_flop}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -430,6 +437,7 @@ def main():
                  "fwd_mesh1m_causal": "tile_fwd(mesh1m-causal-outlier)",
                  "merge": "lse_merge(16x4096x32x128)",
                  "bwd": "tile_bwd(causal-64k)",
+                 "bwd_striped": "tile_bwd(striped-causal-64k)",
                  "chunks": f"{args.chunks} chunk_fwd({head_cfg.name})"}
     line = {
         "metric": "tile attention fwd TFLOP/s on 1 MI355X + % of bf16 MFMA "
