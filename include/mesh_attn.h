@@ -34,8 +34,9 @@
  *    upload, polled without waiting).
  *  - Arguments are validated on the host before anything is enqueued.  On a
  *    non-OK status nothing was launched and mesh_attn_last_error() describes
- *    the problem.  Device work runs asynchronously on `stream`; a launch
- *    failure returns MA_ERR_HIP.
+ *    the problem.  Device work runs asynchronously on `stream`, which must
+ *    belong to the current device (the work-list copy and its event are
+ *    made there); a launch failure returns MA_ERR_HIP.
  */
 #ifndef MESH_ATTN_H
 #define MESH_ATTN_H

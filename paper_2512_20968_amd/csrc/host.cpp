@@ -252,10 +252,17 @@ struct Side {
   int32_t grid = 0;
 };
 
+// An event recorded after a copy, with the device it belongs to (an event
+// can only be recorded on a stream of the device it was created on).
+struct PendingEvent {
+  hipEvent_t ev;
+  int dev;
+};
+
 struct PinnedBuf {
   void* host = nullptr;
   size_t cap = 0;
-  std::vector<hipEvent_t> pending;  // recorded after copies from this buffer
+  std::vector<PendingEvent> pending;  // recorded after copies from this buffer
 };
 
 struct Plan {
@@ -274,18 +281,18 @@ struct PlanView {
 std::mutex g_plan_mu;
 std::map<std::string, Plan> g_plans;
 std::vector<PinnedBuf*> g_spare;       // buffers of evicted plans
-std::vector<hipEvent_t> g_free_events;  // completed events, ready for reuse
+std::map<int, std::vector<hipEvent_t>> g_free_events;  // per device, completed
 uint64_t g_plan_clock = 0;
 constexpr size_t kMaxPlans = 1024;
 
 // Drops the completed events of `b` (to the free list); true if none remain.
 bool retire_completed(PinnedBuf* b) {
   size_t keep = 0;
-  for (hipEvent_t ev : b->pending) {
-    if (hipEventQuery(ev) == hipSuccess)
-      g_free_events.push_back(ev);
+  for (const PendingEvent& pe : b->pending) {
+    if (hipEventQuery(pe.ev) == hipSuccess)
+      g_free_events[pe.dev].push_back(pe.ev);
     else
-      b->pending[keep++] = ev;
+      b->pending[keep++] = pe;
   }
   b->pending.resize(keep);
   return keep == 0;
@@ -494,20 +501,24 @@ ma_status_t upload_plan(int pass, const ma_problem_t* p, const int32_t* q_idx,
   hipError_t e = hipMemcpyAsync(ws, plan.buf->host, plan.bytes,
                                 hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(work list)");
+  int dev = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::vector<hipEvent_t>& pool = g_free_events[dev];
   hipEvent_t ev;
-  if (!g_free_events.empty()) {
-    ev = g_free_events.back();
-    g_free_events.pop_back();
+  if (!pool.empty()) {
+    ev = pool.back();
+    pool.pop_back();
   } else {
     e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
   }
   e = hipEventRecord(ev, stream);
   if (e != hipSuccess) {
-    g_free_events.push_back(ev);
+    pool.push_back(ev);
     return hip_fail(e, "hipEventRecord(work list)");
   }
-  plan.buf->pending.push_back(ev);
+  plan.buf->pending.push_back(PendingEvent{ev, dev});
   view->bytes = plan.bytes;
   view->a = plan.a;
   view->b = plan.b;
