@@ -1,13 +1,10 @@
 """Every row and head of the large forward tiles against the float64 oracle.
 
-The causal 64K tile (16384 rows x 32 heads, 8.8 TFLOP of float64 oracle
-work) runs by default: the oracle's row function is spread over the host
-cores, one (head, row chunk) per worker task, which takes well under a
-minute on 16 cores.  The 1M-token tiles need about eight times that work and
-run only when MESH_ATTN_FULL_TILE names them (a comma list, e.g.
-"mesh1m-nc-gqa,mesh1m-causal-outlier")."""
+The oracle's row function is spread over the host cores, one (head, row
+chunk) per worker task: the causal 64K tile (16384 rows x 32 heads) takes
+well under a minute on 16 cores, each 1M-token tile (65536 rows x 32 heads)
+about a minute and a half."""
 
-import os
 import time
 
 import numpy as np
@@ -20,15 +17,11 @@ from helpers import check_fwd, log, oracle_forward_rows, run_fwd, to_np
 
 pytestmark = pytest.mark.gpu
 
-OPT_IN = ("mesh1m-nc-gqa", "mesh1m-causal-outlier")
+LARGE = ("mesh1m-nc-gqa", "mesh1m-causal-outlier")
 
 
-@pytest.mark.parametrize("name", ["causal-64k", *OPT_IN])
+@pytest.mark.parametrize("name", ["causal-64k", *LARGE])
 def test_every_row_every_head(gpu, name):
-    if name in OPT_IN and name not in os.environ.get(
-            "MESH_ATTN_FULL_TILE", "").split(","):
-        pytest.skip(f"{name}: full-tile oracle run is opt-in "
-                    "(MESH_ATTN_FULL_TILE=<workload names>)")
     cfg = WORKLOADS[name]
     q, k, v, _ = make_qkv(cfg)
     qd, kd, vd = (t.to(gpu) for t in (q, k, v))
@@ -40,9 +33,11 @@ def test_every_row_every_head(gpu, name):
     worst_o = worst_l = 0.0
     t0 = time.time()
     # Eight heads per oracle batch keeps the float64 results of a batch at a
-    # few GB.
-    for h0 in range(0, cfg.num_q_heads, 8):
-        heads = list(range(h0, min(cfg.num_q_heads, h0 + 8)))
+    # few GB; four on the 1M-token tiles, so that a progress line comes
+    # every few seconds.
+    per = 4 if name in LARGE else 8
+    for h0 in range(0, cfg.num_q_heads, per):
+        heads = list(range(h0, min(cfg.num_q_heads, h0 + per)))
         ro, rl = oracle_forward_rows(cfg.problem(), cfg.q_idx, cfg.kv_idx, q,
                                      k, v, rows, heads)
         eo, el = check_fwd(f"{name} heads {heads[0]}..{heads[-1]} "
