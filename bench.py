@@ -25,6 +25,9 @@ resident in HBM (all bf16, head_dim 128):
                    (mesh_attn_chunk_fwd, float32 running partials).
   bwd_striped      (not in the default step) the backward of the striped
                    64K tile (dO from seed 6).
+  bwd_gqa          (not in the default step) the backward of the 1M-token
+                   non-causal GQA tile (32 query heads on 8 KV heads, dO
+                   from seed 8).
 
 `value` is the headline tile's forward TFLOP/s: algorithmic FLOPs
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
@@ -36,6 +39,7 @@ stderr.
 """
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -50,7 +54,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 DEFAULT_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
                 "chunks")
-ALL_LEGS = DEFAULT_LEGS + ("bwd_striped",)
+ALL_LEGS = DEFAULT_LEGS + ("bwd_striped", "bwd_gqa")
 
 
 def log(msg):
@@ -258,6 +262,11 @@ def main():
         t = Tile(ma, WORKLOADS["striped-causal-64k"], dev, with_bwd=True)
         t.fwd(ma)
         tiles["bwd_striped"] = t
+    if "bwd_gqa" in legs:
+        gcfg = dataclasses.replace(WORKLOADS["mesh1m-nc-gqa"], grad_seed=8)
+        t = Tile(ma, gcfg, dev, with_bwd=True)
+        t.fwd(ma)
+        tiles["bwd_gqa"] = t
     if "chunks" in legs:
         # The buffers the chunk all-gathers would produce (chunk i of every
         # Q partition, chunk j of every KV partition), built before timing.
@@ -304,7 +313,7 @@ def main():
         for name in legs:
             if name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
                 leg(name, ev, lambda: tiles[name].fwd(ma))
-            elif name in ("bwd", "bwd_striped"):
+            elif name in ("bwd", "bwd_striped", "bwd_gqa"):
                 leg(name, ev, lambda: tiles[name].bwd(ma))
             elif name == "merge":
                 leg(name, ev, lambda: ma.mesh_attn_lse_merge(
@@ -412,13 +421,13 @@ def main():
                              "bytes": mbytes,
                              "shape": f"k={mk} x {mrows} rows x {mh} heads x "
                                       f"{md}, bf16 in/out"}
-    for name in ("bwd", "bwd_striped"):
+    for name in ("bwd", "bwd_striped", "bwd_gqa"):
         if name not in legs:
             continue
         t = tiles[name]
         tb = t.bwd_flop / (leg_ms[name] * 1e-3) / 1e12
-        out_legs[name] = {"workload": ("bwd-causal-64k" if name == "bwd"
-                                       else t.cfg.name),
+        wl = {"bwd": "bwd-causal-64k", "bwd_gqa": "bwd-mesh1m-nc-gqa"}
+        out_legs[name] = {"workload": wl.get(name, t.cfg.name),
                           "ms": round(leg_ms[name], 4),
                           "ms_median": round(leg_med[name], 4),
                           "tflops": round(tb, 2),
@@ -438,6 +447,7 @@ def main():
                  "merge": "lse_merge(16x4096x32x128)",
                  "bwd": "tile_bwd(causal-64k)",
                  "bwd_striped": "tile_bwd(striped-causal-64k)",
+                 "bwd_gqa": "tile_bwd(mesh1m-nc-gqa)",
                  "chunks": f"{args.chunks} chunk_fwd({head_cfg.name})"}
     line = {
         "metric": "tile attention fwd TFLOP/s on 1 MI355X + % of bf16 MFMA "
