@@ -226,7 +226,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the library runs on one GPU (asked for "
-              f"--gpus {args.gpus}); this build has no multi-GPU path.",
+              f"--gpus {args.gpus}); it has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
     legs = [x for x in args.legs.split(",") if x]
