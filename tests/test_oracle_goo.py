@@ -70,6 +70,17 @@ def test_nonuniform_costs_higher_index_chunk_wins(case):
     assert steps == _golden_steps(case)
 
 
+@pytest.mark.parametrize("case", json.load(open(GOLDEN_NU))["cases"],
+                         ids=lambda c: c["name"])
+def test_nonuniform_makespan(case):
+    """plan_makespan of the hand-derived schedules equals their makespan
+    worked out by hand (steps back to back, each as long as the longer of
+    its collective and its tasks)."""
+    steps = _golden_steps(case)
+    assert goo.plan_makespan(steps, case["t_ag_q"], case["t_ag_kv"],
+                             case["t_rs_q"], case["t_c"]) == case["makespan"]
+
+
 def test_every_chunk_is_a_candidate():
     """On random unequal costs the chosen collective always has the highest
     profit among all schedulable chunks (not only the lowest-index ones)."""
