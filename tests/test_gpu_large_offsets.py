@@ -108,3 +108,36 @@ def test_dkdv_identities_past_int32_offsets(big):
     log(f"large offsets: max |sum dK| / sum|dK| = {rk:.3e}, "
         f"max |sum dV - sum dO| / sum|dV| = {rv:.3e}")
     assert rk <= 1e-2 and rv <= 1e-2
+
+
+def test_merge_past_int32_offsets(gpu):
+    """LSE merge of 16 bf16 partials of 33000 rows x 32 heads x 128 (2.16e9
+    elements): rows whose last-partial elements lie past 2^31 (and a few
+    before) against the oracle's reducer, O compared with the oracle's result
+    rounded to bf16."""
+    from oracle.attention import lse_merge
+    k, rows, h, d = 16, 33000, 32, 128
+    assert k * rows * h * d > 2 ** 31
+    g = torch.Generator(device=gpu).manual_seed(54)
+    o_parts = torch.randn((k, rows, h, d), generator=g, device=gpu,
+                          dtype=torch.bfloat16)
+    lse_parts = (torch.randn((k, h, rows), generator=g, device=gpu) * 4
+                 + 10).float()
+    o = torch.empty((rows, h, d), dtype=torch.bfloat16, device=gpu)
+    lse = torch.empty((h, rows), dtype=torch.float32, device=gpu)
+    ma.mesh_attn_lse_merge(o_parts, lse_parts, o, lse)
+    torch.cuda.synchronize()
+    # First row of the last partial whose elements start past 2^31.
+    edge = (2 ** 31 - (k - 1) * rows * h * d) // (h * d)
+    sel = sorted({0, edge - 1, edge, edge + 1, rows - 1,
+                  *np.random.default_rng(55).integers(edge, rows, 16).tolist()})
+    idx = torch.tensor(sel, device=gpu)
+    op = to_np(o_parts[:, idx]).astype(np.float64)     # [k, n, h, d]
+    lp = to_np(lse_parts[:, :, idx]).astype(np.float64)  # [k, h, n]
+    ro = np.zeros((len(sel), h, d))
+    rl = np.zeros((h, len(sel)))
+    for hh in range(h):
+        ro[:, hh], rl[hh] = lse_merge(op[:, :, hh], lp[:, hh])
+    ro_bf16 = to_np(torch.from_numpy(ro).to(torch.bfloat16))
+    check_fwd(f"large-offset merge, {len(sel)} rows x {h} heads",
+              to_np(o[idx]), to_np(lse[:, idx]), ro_bf16, rl)
