@@ -215,6 +215,30 @@ def test_causal64k_backward_sampled_rows(bwd64k, heads):
                    rdv[:, i])
 
 
+def test_causal64k_head_dim64_backward_sampled(gpu):
+    """The head_dim 64 backward kernels on the full-size causal 64K tile:
+    dQ on the sampled Q rows and dK, dV on the sampled KV rows of every head
+    against the float64 oracle."""
+    cfg = dataclasses.replace(WORKLOADS["bwd-causal-64k"], head_dim=64,
+                              name="bwd-causal-64k-d64")
+    b = _gpu_backward_cpu(cfg, gpu)
+    heads = list(range(cfg.num_q_heads))
+    q_rows = sample_rows(cfg, cfg.nq)
+    kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000)
+    log(f"causal-64k d64 backward: oracle on all {len(heads)} heads")
+    rdq, rdk, rdv, q_heads = oracle_backward_rows(
+        b["prob"], cfg.q_idx, cfg.kv_idx, b["q"], b["k"], b["v"], b["do"],
+        heads, q_rows, kv_rows)
+    assert q_heads == heads
+    for i, h in enumerate(heads):
+        check_grad(f"causal-64k d64 dq h{h}", to_np(b["dq"][q_rows][:, h]),
+                   rdq[:, i])
+        check_grad(f"causal-64k d64 dk h{h}", to_np(b["dk"][kv_rows][:, h]),
+                   rdk[:, i])
+        check_grad(f"causal-64k d64 dv h{h}", to_np(b["dv"][kv_rows][:, h]),
+                   rdv[:, i])
+
+
 def test_mesh1m_gqa_backward_identities_and_dq(bwd1m):
     """Backward at the 1M-token non-causal GQA tile's full size (65536 rows,
     32 query heads on 8 KV heads).  On every KV head, the identities that

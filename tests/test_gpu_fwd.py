@@ -104,6 +104,13 @@ def test_causal64k_sampled(gpu):
     _sampled_parity(WORKLOADS["causal-64k"], gpu)
 
 
+def test_causal64k_head_dim64_sampled(gpu):
+    """The head_dim 64 kernel (its own swizzles and load shapes) on the
+    full-size causal 64K tile, sampled rows of every head."""
+    _sampled_parity(dataclasses.replace(WORKLOADS["causal-64k"], head_dim=64,
+                                        name="causal-64k-d64"), gpu)
+
+
 def test_mesh1m_nc_gqa_sampled(gpu):
     _sampled_parity(WORKLOADS["mesh1m-nc-gqa"], gpu)
 
