@@ -99,3 +99,41 @@ def test_noalloc_rejects_tiles_beyond_its_scratch():
     # the usual argument checks still apply
     assert call(dict(base, head_dim=96), 1, 1) == \
         ma._binding.MA_ERR_UNSUPPORTED
+
+
+@pytest.mark.gpu
+def test_noalloc_forward_in_a_captured_graph(gpu):
+    """The allocation-free forward captured into a HIP graph (two kernel
+    launches and nothing else) and replayed three times.  Before each replay
+    the outputs are overwritten and an eager allocation-free forward of
+    another tile rewrites the shared scratch array, so the replay has to
+    rebuild its own work list; every replay must reproduce the eager forward
+    bit for bit."""
+    cfg = dataclasses.replace(WORKLOADS["tiny-nc"], causal=True, seed=63,
+                              partition_len=1024, num_partitions=4,
+                              q_idx=[3, 1], kv_idx=[0, 1, 3])
+    other = dataclasses.replace(cfg, q_idx=[2], kv_idx=[2, 0], seed=64)
+    q, k, v, _ = make_qkv(cfg)
+    qd, kd, vd = (t.to(gpu) for t in (q, k, v))
+    q2, k2, v2, _ = make_qkv(other)
+    q2d, k2d, v2d = (t.to(gpu) for t in (q2, k2, v2))
+    prob = cfg.problem()
+    P, hq, d = cfg.partition_len, cfg.num_q_heads, cfg.head_dim
+    ref_o, ref_l = _noalloc(prob, cfg, qd, kd, vd, torch.bfloat16)  # eager
+    torch.cuda.synchronize()
+    o = torch.empty((cfg.nq * P, hq, d), dtype=torch.bfloat16, device=gpu)
+    lse = torch.empty((hq, cfg.nq * P), dtype=torch.float32, device=gpu)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        ma.mesh_attn_tile_fwd_noalloc(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd,
+                                      o, lse)
+    for rep in range(3):
+        o.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        _noalloc(other.problem(), other, q2d, k2d, v2d, torch.float32)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o, ref_o), f"replay {rep}: O differs"
+        assert torch.equal(lse, ref_l), f"replay {rep}: LSE differs"
+    log("noalloc forward: three graph replays equal the eager forward")
