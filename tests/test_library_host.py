@@ -243,3 +243,44 @@ def test_struct_layouts_match_the_header(tmp_path):
     assert [f for f, _ in ma.Problem._fields_] == [
         "num_partitions", "partition_len", "num_q_heads", "num_kv_heads",
         "head_dim", "causal", "layout", "softmax_scale"]
+
+
+def test_concurrent_host_calls_and_thread_local_errors():
+    """Eight threads call the work-list builders at once (ctypes releases the
+    GIL, so the library runs them concurrently) and each provokes its own
+    error: every list equals the single-threaded one, and every thread reads
+    its own last-error text (the text is per thread)."""
+    import threading
+    prob = _prob(num_partitions=16, partition_len=512)
+    q_idx, kv_idx = [9, 3, 12], [0, 5, 9, 12, 15]
+    ref = ma.mesh_attn_worklist(prob, q_idx, kv_idx, 128, 64)
+    ref_kv = ma.mesh_attn_worklist_kv_major(prob, q_idx, kv_idx, 128, 64)
+    failures = []
+    start = threading.Barrier(8)
+
+    def work(t):
+        try:
+            start.wait()
+            for it in range(40):
+                ptr, runs = ma.mesh_attn_worklist(prob, q_idx, kv_idx, 128, 64)
+                assert np.array_equal(ptr, ref[0])
+                assert np.array_equal(runs, ref[1])
+                ptr, runs = ma.mesh_attn_worklist_kv_major(prob, q_idx, kv_idx,
+                                                           128, 64)
+                assert np.array_equal(ptr, ref_kv[0])
+                assert np.array_equal(runs, ref_kv[1])
+                bad = 100 + 8 * it + t
+                with pytest.raises(ma.MeshAttnError) as ei:
+                    ma.mesh_attn_worklist(prob, [bad], kv_idx, 128, 64)
+                want = f"= {bad} outside [0, 16)"
+                assert want in ei.value.args[0], ei.value.args[0]
+                assert want in ma.mesh_attn_last_error()
+        except Exception as e:  # collected and re-raised in the main thread
+            failures.append(f"thread {t}: {e!r}")
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(8)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not failures, failures
