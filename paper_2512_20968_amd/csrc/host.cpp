@@ -248,8 +248,9 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Side {
-  size_t off_ptr = 0, off_runs = 0, off_order = 0;
+  size_t off_ptr = 0, off_runs = 0, off_order = 0, off_queue = 0;
   int32_t grid = 0;
+  int32_t n_items = 0;  // non-idle slots of the order
 };
 
 // An event recorded after a copy, with the device it belongs to (an event
@@ -422,7 +423,7 @@ struct SideData {
 
 size_t side_bytes(const SideData& s) {
   return align_up(s.ptr.size() * 4) + align_up(s.runs.size() * sizeof(DevRun)) +
-         align_up(s.order.size() * sizeof(int2));
+         align_up(s.order.size() * sizeof(int2)) + align_up(kNumXcd * 4);
 }
 
 void side_pack(const SideData& s, char* base, size_t off, Side* out) {
@@ -436,7 +437,14 @@ void side_pack(const SideData& s, char* base, size_t off, Side* out) {
   out->off_order = off;
   if (!s.order.empty())
     std::memcpy(base + off, s.order.data(), s.order.size() * sizeof(int2));
+  off += align_up(s.order.size() * sizeof(int2));
+  // The forward's item counters, one per XCD lane, uploaded as zeros with
+  // every call.
+  out->off_queue = off;
+  std::memset(base + off, 0, kNumXcd * 4);
   out->grid = static_cast<int32_t>(s.order.size());
+  out->n_items = 0;
+  for (const int2& it : s.order) out->n_items += it.x >= 0;
 }
 
 // Upper bound of one side's packed bytes from sizes alone (at most two
@@ -445,7 +453,8 @@ void side_pack(const SideData& s, char* base, size_t off, Side* out) {
 size_t side_bound(int64_t n_blocks, int64_t n_list, int64_t heads) {
   return align_up((n_blocks + 1) * 4) +
          align_up(n_blocks * n_list * 2 * sizeof(DevRun)) +
-         align_up((n_blocks * heads + kNumXcd) * sizeof(int2));
+         align_up((n_blocks * heads + kNumXcd) * sizeof(int2)) +
+         align_up(kNumXcd * 4);
 }
 
 constexpr ma_chunk_t kWholeTile{0, 1, 0, 1};
@@ -604,6 +613,8 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   fp.qblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan.a.off_ptr);
   fp.runs = reinterpret_cast<const DevRun*>(wsb + plan.a.off_runs);
   fp.order = reinterpret_cast<const int2*>(wsb + plan.a.off_order);
+  fp.queue = reinterpret_cast<int32_t*>(wsb + plan.a.off_queue);
+  fp.n_items = plan.a.n_items;
   fp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
   fp.hq = prob->num_q_heads;
   fp.hkv = prob->num_kv_heads;
@@ -611,7 +622,9 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   fp.scale_log2 = prob->softmax_scale * kLog2e;
   fp.accumulate = accumulate;
   if (plan.a.grid == 0) return ok();  // cannot happen: every block is listed
-  hipError_t e = launch_tile_fwd(fp, prob->head_dim, o_f32, plan.a.grid, stream);
+  hipError_t e = launch_tile_fwd(
+      fp, prob->head_dim, o_f32,
+      static_cast<int>(fwd_launch_grid(plan.a.n_items)), stream);
   if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
   return ok();
 }
@@ -871,6 +884,8 @@ ma_status_t mesh_attn_tile_fwd_noalloc(const ma_problem_t* prob,
   bp.qblk_ptr = reinterpret_cast<int32_t*>(base);
   bp.runs = reinterpret_cast<DevRun*>(base + off_runs);
   bp.order = reinterpret_cast<int2*>(base + off_order);
+  bp.queue = reinterpret_cast<int32_t*>(
+      base + off_order + align_up(static_cast<size_t>(grid) * sizeof(int2)));
   for (int32_t i = 0; i < nq; ++i) bp.q_idx[i] = q_idx[i];
   for (int32_t i = 0; i < nkv; ++i) bp.kv_idx[i] = kv_idx[i];
   e = launch_fwd_plan_build(bp, stream);
@@ -884,13 +899,16 @@ ma_status_t mesh_attn_tile_fwd_noalloc(const ma_problem_t* prob,
   fp.qblk_ptr = bp.qblk_ptr;
   fp.runs = bp.runs;
   fp.order = bp.order;
+  fp.queue = bp.queue;
+  fp.n_items = static_cast<int32_t>(items);
   fp.rows_q = int64_t{nq} * prob->partition_len;
   fp.hq = prob->num_q_heads;
   fp.hkv = prob->num_kv_heads;
   fp.group = bp.group;
   fp.scale_log2 = prob->softmax_scale * kLog2e;
   fp.accumulate = 0;
-  e = launch_tile_fwd(fp, prob->head_dim, o_dtype == MA_FP32, bp.grid, stream);
+  e = launch_tile_fwd(fp, prob->head_dim, o_dtype == MA_FP32,
+                      static_cast<int>(fwd_launch_grid(items)), stream);
   if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
   return ok();
 }

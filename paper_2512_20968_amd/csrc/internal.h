@@ -39,12 +39,36 @@ struct FwdParams {
   float* lse;          // [hq][rows_q]
   const int32_t* qblk_ptr;   // [n_qblk + 1]
   const DevRun* runs;
-  const int2* order;         // [grid] (qblk, q head); qblk < 0: idle slot
+  const int2* order;         // (qblk, q head); XCD lane x at slots j*8 + x
+  int32_t* queue;            // [8] items taken from each lane; 0 at launch
+  int32_t n_items;           // items (Q block, q head) in the order
   int64_t rows_q;
   int32_t hq, hkv, group;
   float scale_log2;    // softmax scale * log2(e)
   int32_t accumulate;  // 1: fold into the float32 (O, LSE) already stored
 };
+
+// Forward workgroups.  The XCDs of the part run at different speeds (a few
+// per cent apart under load) while the dispatcher gives each an eighth of
+// the workgroups, so on tiles with many items per compute unit the last
+// quarter of every XCD lane of the order is taken from per-lane counters:
+// the first fwd_static_slots(n) workgroups take slot blockIdx.x, the others
+// the next remaining item of their XCD's lane or else of another lane, and
+// about one in eight more of them are launched than remaining items, so an
+// XCD that runs faster takes more of the last items.  Below
+// kFwdDynamicMinItems (16 items per compute unit of the 256-CU part) every
+// whole row of eight slots is static.
+constexpr int64_t kFwdDynamicMinItems = 4096;
+__host__ __device__ inline int64_t fwd_static_slots(int64_t n_items) {
+  return n_items >= kFwdDynamicMinItems ? (n_items / 8) * 3 / 4 * 8
+                                        : (n_items / 8) * 8;
+}
+__host__ __device__ inline int64_t fwd_launch_grid(int64_t n_items) {
+  const int64_t fixed = fwd_static_slots(n_items);
+  const int64_t dyn = n_items - fixed;
+  const int64_t extra = n_items >= kFwdDynamicMinItems ? dyn / 8 + 8 : 0;
+  return fixed + (dyn + extra + 7) / 8 * 8;
+}
 
 hipError_t launch_tile_fwd(const FwdParams& p, int head_dim, bool out_f32,
                            int grid, hipStream_t stream);
@@ -109,6 +133,7 @@ struct PlanBuildParams {
   int32_t* qblk_ptr;              // [nqb + 1] in the scratch array
   DevRun* runs;                   // [<= 2 nqb nkv]
   int2* order;                    // [grid]
+  int32_t* queue;                 // [8] lane counters, zeroed by the build
   int32_t q_idx[kNoAllocMaxList];
   int32_t kv_idx[kNoAllocMaxList];
 };

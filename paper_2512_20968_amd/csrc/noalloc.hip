@@ -163,6 +163,7 @@ __global__ __launch_bounds__(kBuildThreads) void fwd_plan_build_kernel(
   }
   for (int slot = p.nqb * p.hq + t; slot < p.grid; slot += kBuildThreads)
     p.order[slot] = make_int2(-1, -1);
+  if (t < kNumXcd) p.queue[t] = 0;
 }
 
 // Device address of the scratch array, per device (each GPU holds its own

@@ -118,8 +118,36 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  const int2 item = load_const(p.order, blockIdx.x);
-  if (item.x < 0) return;
+  // Item.  Workgroups below the static count take slot blockIdx.x of the
+  // order (lane x of XCD x at slots j * 8 + x).  The others take the next
+  // remaining item of their XCD's lane, else of another lane: the launch has
+  // more of them than remaining items, so an XCD that runs faster takes more
+  // of the last items; one that finds every lane taken has nothing to do.  A
+  // plain read of a lane's counter skips a taken lane without an atomic.
+  const int n_static = static_cast<int>(fwd_static_slots(p.n_items));
+  int slot = static_cast<int>(blockIdx.x);
+  if (slot >= n_static) {
+    int* s_slot = reinterpret_cast<int*>(smem + L::SMEM);
+    if (threadIdx.x == 0) {
+      const int x = static_cast<int>(blockIdx.x % kNumXcd);
+      const int j0 = n_static / kNumXcd;  // positions taken statically
+      int got = -1;
+      for (int t = 0; t < kNumXcd && got < 0; ++t) {
+        const int y = (x + t) % kNumXcd;
+        const int len = (p.n_items - y + kNumXcd - 1) / kNumXcd - j0;
+        if (__hip_atomic_load(&p.queue[y], __ATOMIC_RELAXED,
+                              __HIP_MEMORY_SCOPE_AGENT) >= len)
+          continue;
+        const int c = atomicAdd(&p.queue[y], 1);
+        if (c < len) got = (j0 + c) * kNumXcd + y;
+      }
+      *s_slot = got;
+    }
+    __syncthreads();
+    slot = __builtin_amdgcn_readfirstlane(*s_slot);
+    if (slot < 0) return;
+  }
+  const int2 item = load_const(p.order, slot);
   const int qblk = item.x;
   const int h = item.y;
   const int hk = h / p.group;
@@ -503,7 +531,7 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
 
 template <int D, bool F32>
 hipError_t launch(const FwdParams& p, int grid, hipStream_t stream) {
-  const size_t smem = FwdLayout<D>::SMEM;
+  const size_t smem = FwdLayout<D>::SMEM + 16;  // + the item slot
   const hipError_t e = ensure_dynamic_lds<tile_fwd_kernel<D, F32>>(smem);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((tile_fwd_kernel<D, F32>), dim3(grid), dim3(NT), smem,
