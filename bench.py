@@ -89,10 +89,14 @@ def visible_pairs(cfg, q_rows=None):
 
 
 def source_digest(names):
+    """Digest of the named kernel sources and of the build script, whose
+    compile flags shape the kernels too."""
     h = hashlib.sha256()
-    for n in names:
-        with open(os.path.join(ROOT, "paper_2512_20968_amd", "csrc", n),
-                  "rb") as f:
+    paths = [os.path.join(ROOT, "paper_2512_20968_amd", "csrc", n)
+             for n in names]
+    paths.append(os.path.join(ROOT, "paper_2512_20968_amd", "build.py"))
+    for path in paths:
+        with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 

@@ -28,7 +28,11 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # Per-file additions.  The backward kernels keep dK, dV (or dQ) and the score
 # tiles live together; MFMA results in VGPR form keep the compiler from
 # parking score accumulators in AGPRs and copying them back for the softmax.
-EXTRA = {"tile_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# The forward is scheduled with the target's own register-pressure trackers:
+# its float32-output kernel then fits 256 registers without a spill, and the
+# bf16-output kernel's schedule runs 0.5-1.6 % faster.
+EXTRA = {"tile_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "tile_fwd.hip": ["-mllvm", "-amdgpu-use-amdgpu-trackers"]}
 
 
 def hipcc():
