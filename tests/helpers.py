@@ -17,6 +17,21 @@ LSE_TOL = 1e-3
 GRAD_REL_TOL = 5e-2
 
 
+def queued_tail_config():
+    """A causal tile of 4137 forward items (197 Q blocks of 256 rows x 21
+    query heads): more than the 4096 items from which the forward takes the
+    last quarter of every XCD lane from per-lane counters, an item count that
+    is not a multiple of 8, and 7 KV heads (so the plain item order rather
+    than the KV-head-per-XCD one).  Q partitions 3..199 against KV partitions
+    0, 100 and 199 of 256 tokens: FULL, PARTIAL and EMPTY block pairs."""
+    import dataclasses
+    from mesh_inputs import WORKLOADS
+    return dataclasses.replace(
+        WORKLOADS["tiny-nc"], name="queued-tail", num_partitions=200,
+        partition_len=256, q_idx=list(range(3, 200)), kv_idx=[0, 100, 199],
+        num_q_heads=21, num_kv_heads=7, head_dim=64, causal=True, seed=63)
+
+
 def log(msg):
     print(f"[{time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 

@@ -11,7 +11,8 @@ import oracle
 import paper_2512_20968_amd as ma
 from mesh_inputs import WORKLOADS, make_merge_parts, make_qkv, sample_rows
 
-from helpers import check_fwd, log, oracle_forward_rows, run_fwd, to_np
+from helpers import (check_fwd, log, oracle_forward_rows, queued_tail_config,
+                     run_fwd, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -113,6 +114,33 @@ def test_causal64k_head_dim64_sampled(gpu):
 
 def test_mesh1m_nc_gqa_sampled(gpu):
     _sampled_parity(WORKLOADS["mesh1m-nc-gqa"], gpu)
+
+
+def test_queued_items_ragged_tail_plain_order(gpu):
+    """The work-queue path with a ragged tail (queued_tail_config): O and LSE
+    start as NaN, so an item that no workgroup took would stay NaN; sampled
+    rows of every head against the oracle."""
+    cfg = queued_tail_config()
+    assert cfg.nq * cfg.num_q_heads >= 4096
+    assert (cfg.nq * cfg.num_q_heads) % 8 != 0 and cfg.num_kv_heads % 8 != 0
+    (q, k, v), (qd, kd, vd), _ = _inputs(cfg, gpu)
+    prob = cfg.problem()
+    P, hq, d = cfg.partition_len, cfg.num_q_heads, cfg.head_dim
+    o = torch.full((cfg.nq * P, hq, d), float("nan"), dtype=torch.bfloat16,
+                   device=gpu)
+    lse = torch.full((hq, cfg.nq * P), float("nan"), dtype=torch.float32,
+                     device=gpu)
+    log(f"{cfg.name}: launching forward ({cfg.nq * hq} items)")
+    ma.mesh_attn_tile_fwd(prob, cfg.q_idx, cfg.kv_idx, qd, kd, vd, o, lse)
+    torch.cuda.synchronize()
+    assert not torch.isnan(o).any() and not torch.isnan(lse).any()
+    rows = sample_rows(cfg, cfg.nq, n_random=2)
+    heads = list(range(hq))
+    ro, rl = oracle_forward_rows(prob, cfg.q_idx, cfg.kv_idx, q, k, v, rows,
+                                 heads)
+    idx = torch.tensor(rows, device=gpu)
+    check_fwd(f"{cfg.name} sampled", o[idx].float().cpu().numpy(),
+              lse[:, idx].cpu().numpy(), ro, rl)
 
 
 def test_mesh1m_causal_outlier_sampled(gpu):

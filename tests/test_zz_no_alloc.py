@@ -19,7 +19,7 @@ import oracle
 import paper_2512_20968_amd as ma
 from mesh_inputs import WORKLOADS, make_qkv
 
-from helpers import check_fwd, log, run_fwd, to_np
+from helpers import check_fwd, log, queued_tail_config, run_fwd, to_np
 
 
 def _noalloc(prob, cfg, qd, kd, vd, out_dtype):
@@ -64,7 +64,9 @@ def test_noalloc_matches_workspace_forward(gpu):
         q_idx=[3, 0, 2], kv_idx=[1, 3, 0], num_q_heads=8, num_kv_heads=2,
         head_dim=128, causal=True, layout=1, seed=62)
     _case(striped, gpu, torch.bfloat16, check_oracle=True)
-    # 4. The 1M-token GQA tile at full size (8 KV heads), then the tiny one.
+    # 4. Past 4096 items with a ragged tail and the plain item order.
+    _case(queued_tail_config(), gpu, torch.bfloat16)
+    # 5. The 1M-token GQA tile at full size (8 KV heads), then the tiny one.
     _case(WORKLOADS["mesh1m-nc-gqa"], gpu, torch.bfloat16)
     _case(WORKLOADS["tiny-nc"], gpu, torch.bfloat16, check_oracle=True)
 
