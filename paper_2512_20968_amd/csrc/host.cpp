@@ -438,8 +438,8 @@ void side_pack(const SideData& s, char* base, size_t off, Side* out) {
   if (!s.order.empty())
     std::memcpy(base + off, s.order.data(), s.order.size() * sizeof(int2));
   off += align_up(s.order.size() * sizeof(int2));
-  // The forward's item counters, one per XCD lane, uploaded as zeros with
-  // every call.
+  // The item counters of this side's order, one per XCD lane (see
+  // queued_static_slots), uploaded as zeros with every call.
   out->off_queue = off;
   std::memset(base + off, 0, kNumXcd * 4);
   out->grid = static_cast<int32_t>(s.order.size());
@@ -624,7 +624,7 @@ ma_status_t fwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   if (plan.a.grid == 0) return ok();  // cannot happen: every block is listed
   hipError_t e = launch_tile_fwd(
       fp, prob->head_dim, o_f32,
-      static_cast<int>(fwd_launch_grid(plan.a.n_items)), stream);
+      static_cast<int>(queued_launch_grid(plan.a.n_items)), stream);
   if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
   return ok();
 }
@@ -682,6 +682,10 @@ ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   bp.kvblk_ptr = reinterpret_cast<const int32_t*>(wsb + plan.b.off_ptr);
   bp.kvruns = reinterpret_cast<const DevRun*>(wsb + plan.b.off_runs);
   bp.kvorder = reinterpret_cast<const int2*>(wsb + plan.b.off_order);
+  bp.qqueue = reinterpret_cast<int32_t*>(wsb + plan.a.off_queue);
+  bp.kvqueue = reinterpret_cast<int32_t*>(wsb + plan.b.off_queue);
+  bp.q_items = plan.a.n_items;
+  bp.kv_items = plan.b.n_items;
   bp.rows_q = int64_t{nq} * (prob->partition_len / ch.num_q_chunks);
   bp.rows_kv = int64_t{nkv} * (prob->partition_len / ch.num_kv_chunks);
   bp.hq = prob->num_q_heads;
@@ -690,8 +694,11 @@ ma_status_t bwd_impl(const ma_problem_t* prob, const int32_t* q_idx,
   bp.scale = prob->softmax_scale;
   bp.scale_log2 = prob->softmax_scale * kLog2e;
   bp.accumulate = accumulate;
-  hipError_t e =
-      launch_tile_bwd(bp, prob->head_dim, plan.a.grid, plan.b.grid, stream);
+  hipError_t e = launch_tile_bwd(
+      bp, prob->head_dim,
+      plan.a.n_items > 0 ? static_cast<int>(queued_launch_grid(plan.a.n_items)) : 0,
+      plan.b.n_items > 0 ? static_cast<int>(queued_launch_grid(plan.b.n_items)) : 0,
+      stream);
   if (e != hipSuccess) return hip_fail(e, "tile_bwd launch");
   return ok();
 }
@@ -908,7 +915,7 @@ ma_status_t mesh_attn_tile_fwd_noalloc(const ma_problem_t* prob,
   fp.scale_log2 = prob->softmax_scale * kLog2e;
   fp.accumulate = 0;
   e = launch_tile_fwd(fp, prob->head_dim, o_dtype == MA_FP32,
-                      static_cast<int>(fwd_launch_grid(items)), stream);
+                      static_cast<int>(queued_launch_grid(items)), stream);
   if (e != hipSuccess) return hip_fail(e, "tile_fwd launch");
   return ok();
 }

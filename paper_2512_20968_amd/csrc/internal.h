@@ -48,25 +48,25 @@ struct FwdParams {
   int32_t accumulate;  // 1: fold into the float32 (O, LSE) already stored
 };
 
-// Forward workgroups.  The XCDs of the part run at different speeds (a few
-// per cent apart under load) while the dispatcher gives each an eighth of
-// the workgroups, so on tiles with many items per compute unit the last
-// quarter of every XCD lane of the order is taken from per-lane counters:
-// the first fwd_static_slots(n) workgroups take slot blockIdx.x, the others
-// the next remaining item of their XCD's lane or else of another lane, and
-// about one in eight more of them are launched than remaining items, so an
-// XCD that runs faster takes more of the last items.  Below
-// kFwdDynamicMinItems (16 items per compute unit of the 256-CU part) every
-// whole row of eight slots is static.
-constexpr int64_t kFwdDynamicMinItems = 4096;
-__host__ __device__ inline int64_t fwd_static_slots(int64_t n_items) {
-  return n_items >= kFwdDynamicMinItems ? (n_items / 8) * 3 / 4 * 8
-                                        : (n_items / 8) * 8;
+// Workgroup items of the forward and of both backward kernels.  The XCDs of
+// the part run at different speeds (a few per cent apart under load) while
+// the dispatcher gives each an eighth of the workgroups, so on launches with
+// many items per compute unit the last quarter of every XCD lane of the item
+// order is taken from per-lane counters: the first queued_static_slots(n)
+// workgroups take slot blockIdx.x, the others the next remaining item of
+// their XCD's lane or else of another lane, and about one in eight more of
+// them are launched than remaining items, so an XCD that runs faster takes
+// more of the last items.  Below kQueuedMinItems (16 items per compute unit
+// of the 256-CU part) every whole row of eight slots is static.
+constexpr int64_t kQueuedMinItems = 4096;
+__host__ __device__ inline int64_t queued_static_slots(int64_t n_items) {
+  return n_items >= kQueuedMinItems ? (n_items / 8) * 3 / 4 * 8
+                                    : (n_items / 8) * 8;
 }
-__host__ __device__ inline int64_t fwd_launch_grid(int64_t n_items) {
-  const int64_t fixed = fwd_static_slots(n_items);
+__host__ __device__ inline int64_t queued_launch_grid(int64_t n_items) {
+  const int64_t fixed = queued_static_slots(n_items);
   const int64_t dyn = n_items - fixed;
-  const int64_t extra = n_items >= kFwdDynamicMinItems ? dyn / 8 + 8 : 0;
+  const int64_t extra = n_items >= kQueuedMinItems ? dyn / 8 + 8 : 0;
   return fixed + (dyn + extra + 7) / 8 * 8;
 }
 
@@ -106,6 +106,11 @@ struct BwdParams {
   const int32_t* kvblk_ptr;
   const DevRun* kvruns;
   const int2* kvorder;   // (kvblk, kv head)
+  // Per-XCD-lane item counters of the two orders, 0 at launch, and their
+  // item counts (see queued_static_slots).
+  int32_t* qqueue;
+  int32_t* kvqueue;
+  int32_t q_items, kv_items;
   int64_t rows_q, rows_kv;
   int32_t hq, hkv, group;
   float scale, scale_log2;

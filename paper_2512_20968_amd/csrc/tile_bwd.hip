@@ -435,8 +435,10 @@ __global__ __launch_bounds__(NT_KV, 1) void bwd_dkdv_kernel(BwdParams p) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
-  const int2 item = load_const(p.kvorder, blockIdx.x);
-  if (item.x < 0) return;
+  const int slot = queued_slot(p.kv_items, p.kvqueue,
+                               reinterpret_cast<int*>(smem + DkdvLayout<D>::SMEM));
+  if (slot < 0) return;
+  const int2 item = load_const(p.kvorder, slot);
   const int kvblk = item.x;
   const int hk = item.y;
   const int run_b = load_const(p.kvblk_ptr, kvblk);
@@ -467,8 +469,10 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  const int2 item = load_const(p.qorder, blockIdx.x);
-  if (item.x < 0) return;
+  const int slot = queued_slot(p.q_items, p.qqueue,
+                               reinterpret_cast<int*>(smem + L::SMEM));
+  if (slot < 0) return;
+  const int2 item = load_const(p.qorder, slot);
   const int qblk = item.x;
   const int h = item.y;
   const int hk = h / p.group;
@@ -631,8 +635,9 @@ __global__ __launch_bounds__(NT, 1) void bwd_dq_kernel(BwdParams p) {
 template <int D>
 hipError_t launch(const BwdParams& p, int grid_q, int grid_kv,
                   hipStream_t stream) {
-  const size_t smem_kv = DkdvLayout<D>::SMEM;
-  const size_t smem_q = DqLayout<D>::SMEM;
+  // + one int for the item slot of a queued workgroup
+  const size_t smem_kv = DkdvLayout<D>::SMEM + 16;
+  const size_t smem_q = DqLayout<D>::SMEM + 16;
   {
     hipError_t e = ensure_dynamic_lds<bwd_dkdv_kernel<D>>(smem_kv);
     if (e == hipSuccess) e = ensure_dynamic_lds<bwd_dq_kernel<D>>(smem_q);

@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "internal.h"
+
 namespace mesh_attn {
 namespace dev {
 
@@ -25,6 +27,37 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;  // four waves
 constexpr int kTileRows = 64;  // rows of a staged tile
+
+// Item slot of this workgroup in an item order of n_items (XCD lane x at
+// slots j * 8 + x): slot blockIdx.x below queued_static_slots(n_items), else
+// the next remaining item of this workgroup's XCD lane, else of another lane;
+// -1 if every lane is taken.  A plain read of a lane's counter skips a taken
+// lane without an atomic.  s_slot is one int of LDS; every thread of the
+// workgroup must call this (it ends at a barrier when it takes the queue).
+__device__ __forceinline__ int queued_slot(int n_items, int32_t* queue,
+                                           int* s_slot) {
+  constexpr int kLanes = 8;  // XCDs
+  const int n_static = static_cast<int>(queued_static_slots(n_items));
+  const int slot = static_cast<int>(blockIdx.x);
+  if (slot < n_static) return slot;
+  if (threadIdx.x == 0) {
+    const int x = static_cast<int>(blockIdx.x % kLanes);
+    const int j0 = n_static / kLanes;  // positions taken statically
+    int got = -1;
+    for (int t = 0; t < kLanes && got < 0; ++t) {
+      const int y = (x + t) % kLanes;
+      const int len = (n_items - y + kLanes - 1) / kLanes - j0;
+      if (__hip_atomic_load(&queue[y], __ATOMIC_RELAXED,
+                            __HIP_MEMORY_SCOPE_AGENT) >= len)
+        continue;
+      const int c = atomicAdd(&queue[y], 1);
+      if (c < len) got = (j0 + c) * kLanes + y;
+    }
+    *s_slot = got;
+  }
+  __syncthreads();
+  return __builtin_amdgcn_readfirstlane(*s_slot);
+}
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b,
                                          const f32x16& c) {

@@ -118,35 +118,10 @@ __global__ __launch_bounds__(NT, 1) void tile_fwd_kernel(FwdParams p) {
   const int li = lane & 31;
   const int lh = lane >> 5;
 
-  // Item.  Workgroups below the static count take slot blockIdx.x of the
-  // order (lane x of XCD x at slots j * 8 + x).  The others take the next
-  // remaining item of their XCD's lane, else of another lane: the launch has
-  // more of them than remaining items, so an XCD that runs faster takes more
-  // of the last items; one that finds every lane taken has nothing to do.  A
-  // plain read of a lane's counter skips a taken lane without an atomic.
-  const int n_static = static_cast<int>(fwd_static_slots(p.n_items));
-  int slot = static_cast<int>(blockIdx.x);
-  if (slot >= n_static) {
-    int* s_slot = reinterpret_cast<int*>(smem + L::SMEM);
-    if (threadIdx.x == 0) {
-      const int x = static_cast<int>(blockIdx.x % kNumXcd);
-      const int j0 = n_static / kNumXcd;  // positions taken statically
-      int got = -1;
-      for (int t = 0; t < kNumXcd && got < 0; ++t) {
-        const int y = (x + t) % kNumXcd;
-        const int len = (p.n_items - y + kNumXcd - 1) / kNumXcd - j0;
-        if (__hip_atomic_load(&p.queue[y], __ATOMIC_RELAXED,
-                              __HIP_MEMORY_SCOPE_AGENT) >= len)
-          continue;
-        const int c = atomicAdd(&p.queue[y], 1);
-        if (c < len) got = (j0 + c) * kNumXcd + y;
-      }
-      *s_slot = got;
-    }
-    __syncthreads();
-    slot = __builtin_amdgcn_readfirstlane(*s_slot);
-    if (slot < 0) return;
-  }
+  // Item (order slot; see queued_static_slots).
+  const int slot = queued_slot(p.n_items, p.queue,
+                               reinterpret_cast<int*>(smem + L::SMEM));
+  if (slot < 0) return;
   const int2 item = load_const(p.order, slot);
   const int qblk = item.x;
   const int h = item.y;

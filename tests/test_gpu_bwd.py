@@ -12,8 +12,8 @@ import oracle
 import paper_2512_20968_amd as ma
 from mesh_inputs import WORKLOADS, make_grad, make_qkv, sample_rows
 
-from helpers import (check_grad, log, oracle_backward_rows, run_fwd,
-                     to_np)
+from helpers import (check_grad, log, oracle_backward_rows, queued_tail_config,
+                     run_fwd, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -212,6 +212,43 @@ def test_causal64k_backward_sampled_rows(bwd64k, heads):
         check_grad(f"causal-64k dk h{h}", to_np(b["dk"][kv_rows][:, h]),
                    rdk[:, i])
         check_grad(f"causal-64k dv h{h}", to_np(b["dv"][kv_rows][:, h]),
+                   rdv[:, i])
+
+
+def test_queued_items_ragged_tail_backward(gpu):
+    """Both backward kernels on the work-queue path with ragged tails and
+    the plain item order (queued_tail_config: 8274 dQ items, 197 x 2 Q
+    blocks of 128 rows x 21 query heads on 7 KV heads).  dQ, dK and dV start
+    as NaN, so an item no workgroup took would show; dQ on sampled rows and
+    dK, dV on sampled KV rows of every head against the oracle."""
+    cfg = dataclasses.replace(queued_tail_config(), grad_seed=64)
+    assert cfg.nq * (cfg.partition_len // 128) * cfg.num_q_heads >= 4096
+    prob, (q, k, v, do), (qd, kd, vd, dod), o, lse = _setup(cfg, gpu)
+    P, hq, hkv, d = (cfg.partition_len, cfg.num_q_heads, cfg.num_kv_heads,
+                     cfg.head_dim)
+    nan = float("nan")
+    init = (torch.full((cfg.nq * P, hq, d), nan, device=gpu),
+            torch.full((cfg.nkv * P, hkv, d), nan, device=gpu),
+            torch.full((cfg.nkv * P, hkv, d), nan, device=gpu))
+    log(f"{cfg.name}: GPU backward")
+    dq, dk, dv = _run_bwd(prob, cfg, qd, kd, vd, o, dod, lse, init=init)
+    torch.cuda.synchronize()
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        assert not torch.isnan(t).any(), f"{name} has unwritten items"
+    q_rows = sample_rows(cfg, cfg.nq, n_random=2)
+    kv_rows = sample_rows(cfg, cfg.nkv, seed_offset=2000, n_random=4)
+    heads = list(range(hkv))
+    log(f"{cfg.name}: oracle on {len(q_rows)} dQ rows, {len(kv_rows)} dK/dV "
+        f"rows, every head")
+    rdq, rdk, rdv, q_heads = oracle_backward_rows(
+        prob, cfg.q_idx, cfg.kv_idx, q, k, v, do, heads, q_rows, kv_rows)
+    dqc, dkc, dvc = dq.cpu(), dk.cpu(), dv.cpu()
+    for i, h in enumerate(q_heads):
+        check_grad(f"queued-tail dq h{h}", to_np(dqc[q_rows][:, h]), rdq[:, i])
+    for i, hk in enumerate(heads):
+        check_grad(f"queued-tail dk h{hk}", to_np(dkc[kv_rows][:, hk]),
+                   rdk[:, i])
+        check_grad(f"queued-tail dv h{hk}", to_np(dvc[kv_rows][:, hk]),
                    rdv[:, i])
 
 
