@@ -1,13 +1,12 @@
-"""Seeded random tiles, forward and backward, every row and head against the
-float64 oracle: partition counts and lengths, Q and KV index lists (subsets
-in any order, overlapping or not), GQA ratios, both head dims, causal or not,
-both layouts, with and without the x8 outlier rows.  Each case is small
-enough for the oracle to take every row; together they cover shapes the
-named workloads do not."""
+"""Forty-eight seeded random tiles, forward and backward, every row and head
+against the float64 oracle: partition counts and lengths (256 to 2048),
+Q and KV index lists (subsets in any order, overlapping or not), GQA ratios,
+both head dims, causal or not, both layouts, with and without the x8
+outlier rows.  Each case is small enough for the oracle to take every row;
+together they cover shapes the named workloads do not."""
 
 import random
 
-import numpy as np
 import pytest
 import torch
 
@@ -25,9 +24,9 @@ HEADS = [(4, 4), (6, 3), (8, 2), (2, 1), (4, 1)]
 def _random_case(i):
     r = random.Random(7000 + i)
     n = r.randint(3, 10)
-    P = r.choice([256, 512, 1024])
-    nq = r.randint(1, min(3, n))
-    nkv = r.randint(1, min(4, n))
+    P = r.choice([256, 512, 1024, 2048])
+    nq = r.randint(1, min(3 if P < 2048 else 2, n))
+    nkv = r.randint(1, min(4 if P < 2048 else 2, n))
     q_idx = r.sample(range(n), nq)
     kv_idx = r.sample(range(n), nkv)
     hq, hkv = r.choice(HEADS)
@@ -37,7 +36,7 @@ def _random_case(i):
                       layout=int(r.random() < 0.4))
 
 
-CASES = [_random_case(i) for i in range(16)]
+CASES = [_random_case(i) for i in range(48)]
 
 
 @pytest.mark.parametrize("cfg", CASES, ids=[c.name for c in CASES])
@@ -65,8 +64,8 @@ def test_random_tile_forward_and_backward(gpu, cfg):
     ro, rl = oracle.tile_forward(prob, cfg.q_idx, cfg.kv_idx, qn, kn, vn)
     check_fwd(f"{cfg.name} bf16 out", to_np(o), to_np(lse), ro, rl)
     check_fwd(f"{cfg.name} f32 out", to_np(o32), to_np(lse32), ro, rl)
-    rdq, rdk, rdv, q_heads = oracle.tile_backward(prob, cfg.q_idx, cfg.kv_idx,
-                                                  qn, kn, vn, don)
+    rdq, rdk, rdv, q_heads, _ = oracle.tile_backward(prob, cfg.q_idx, cfg.kv_idx,
+                                                     qn, kn, vn, don)
     assert list(q_heads) == list(range(hq))
     check_grad(f"{cfg.name} dq", to_np(dq), rdq)
     check_grad(f"{cfg.name} dk", to_np(dk), rdk)
