@@ -36,7 +36,7 @@ constexpr int kTileRows = 64;  // rows of a staged tile
 // workgroup must call this (it ends at a barrier when it takes the queue).
 __device__ __forceinline__ int queued_slot(int n_items, int32_t* queue,
                                            int* s_slot) {
-  constexpr int kLanes = 8;  // XCDs
+  constexpr int kLanes = kNumXcd;
   const int n_static = static_cast<int>(queued_static_slots(n_items));
   const int slot = static_cast<int>(blockIdx.x);
   if (slot < n_static) return slot;
