@@ -26,10 +26,14 @@
  *  - GQA (Section 4.8): query head h reads KV head h / (num_q_heads /
  *    num_kv_heads).
  *  - Device pointers must be 16-byte aligned.  Outputs must not alias inputs.
- *  - A call writes its device workspace on `stream` (the work list, and for
- *    the forward the counters its workgroups take items from) and reads it
- *    back in its kernels, so a workspace serves one call at a time: calls
- *    that may overlap need workspaces of their own.
+ *  - A call writes its device workspace on `stream` (the work list and the
+ *    counters its workgroups take items from) and reads it back in its
+ *    kernels, so a workspace serves one call at a time: calls that may
+ *    overlap need workspaces of their own.  The work list is copied from a
+ *    cached pinned host buffer that the library may reuse for another tile
+ *    after the copy has completed, so calls that take a workspace must not
+ *    be recorded into a graph (stream capture) and replayed;
+ *    mesh_attn_tile_fwd_noalloc is the forward for that case.
  *  - The caller owns every buffer, host and device.  The library never
  *    allocates or frees device memory and never synchronizes a stream or the
  *    device; its only state is a bounded cache of pinned host copies of work
