@@ -14,7 +14,11 @@
 // O += V(n)^T P(n)^T -- and a VALU phase Y(n) -- mask, running max, rescale
 // and the exponentials that make P(n+1).  Group B runs one phase behind
 // group A and every phase ends at a workgroup barrier, so on each SIMD one
-// wave's MFMAs always overlap the other wave's softmax.
+// wave's MFMAs always overlap the other wave's softmax.  Group B also issues
+// the K/V loads, which makes both of its phases the longer ones of their
+// slots, so its waves run at raised issue priority.  On launches with many
+// items, the last items of each XCD's share are taken from per-XCD counters
+// (queued_slot), so that faster XCDs take more of them.
 //
 // Layout choices (64-wide wavefronts, v_mfma_f32_32x32x16_bf16):
 //  * Scores are computed transposed, S^T = K Q^T (A = K rows from LDS,
