@@ -6,7 +6,6 @@ torch is used for device memory and the current stream only.
 import ctypes
 import os
 import threading
-from typing import Sequence
 
 import numpy as np
 

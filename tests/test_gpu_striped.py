@@ -6,7 +6,6 @@ on the order of the two partitions."""
 
 import dataclasses
 
-import numpy as np
 import pytest
 import torch
 
