@@ -28,6 +28,12 @@ resident in HBM (all bf16, head_dim 128):
   bwd_gqa          (not in the default step) the backward of the 1M-token
                    non-causal GQA tile (32 query heads on 8 KV heads, dO
                    from seed 8).
+  fwd_items64 .. fwd_items512  (not in the default step) the forward on 64,
+                   128, 256 or 512 items of equal length (1024 KV blocks
+                   each), i.e. a quarter, half, all or twice all of the 256
+                   compute units busy: the same work per compute unit at
+                   different chip load, which separates the kernel's
+                   efficiency in clock cycles from the clock the chip holds.
 
 `value` is the headline tile's forward TFLOP/s: algorithmic FLOPs
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
@@ -54,7 +60,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 DEFAULT_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
                 "chunks")
-ALL_LEGS = DEFAULT_LEGS + ("bwd_striped", "bwd_gqa")
+ITEM_LEGS = ("fwd_items64", "fwd_items128", "fwd_items256", "fwd_items512")
+FWD_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal") + ITEM_LEGS
+ALL_LEGS = DEFAULT_LEGS + ("bwd_striped", "bwd_gqa") + ITEM_LEGS
 
 
 def log(msg):
@@ -253,6 +261,9 @@ def main():
     if "fwd_mesh1m_causal" in legs:
         tiles["fwd_mesh1m_causal"] = Tile(
             ma, WORKLOADS["mesh1m-causal-outlier"], dev)
+    for name in ITEM_LEGS:
+        if name in legs:
+            tiles[name] = Tile(ma, WORKLOADS[f"items-{name[9:]}"], dev)
     if "bwd" in legs:
         # The backward workload is the backward of the causal 64K tile: same
         # inputs (seed 1), dO from seed 4, O and LSE from its forward, which
@@ -315,7 +326,7 @@ def main():
 
     def run_step(ev=None):
         for name in legs:
-            if name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
+            if name in FWD_LEGS:
                 leg(name, ev, lambda: tiles[name].fwd(ma))
             elif name in ("bwd", "bwd_striped", "bwd_gqa"):
                 leg(name, ev, lambda: tiles[name].bwd(ma))
@@ -371,7 +382,7 @@ def main():
     out_legs = {}
     roofline = None
     value = None
-    for name in ("fwd", "fwd_causal64k", "fwd_mesh1m_causal"):
+    for name in FWD_LEGS:
         if name not in legs:
             continue
         t = tiles[name]
@@ -393,6 +404,12 @@ def main():
                                                   fwd_dig),
                           "worklist_host_ms": round(wl_ms, 3),
                           "worklist_runs": int(len(wl_runs))}
+        if name in ITEM_LEGS:
+            items = int(name[9:])
+            busy = min(items, 256)
+            out_legs[name]["busy_cus"] = busy
+            out_legs[name]["tflops_per_256_busy_cus"] = round(
+                tf * 256 / busy, 2)
         if name == "fwd":
             value = tf
             roofline = {"bound": "mfma", "achieved": round(tf, 2),
@@ -453,6 +470,7 @@ def main():
                  "bwd_striped": "tile_bwd(striped-causal-64k)",
                  "bwd_gqa": "tile_bwd(mesh1m-nc-gqa)",
                  "chunks": f"{args.chunks} chunk_fwd({head_cfg.name})"}
+    step_desc.update({n: f"tile_fwd(items-{n[9:]})" for n in ITEM_LEGS})
     line = {
         "metric": "tile attention fwd TFLOP/s on 1 MI355X + % of bf16 MFMA "
                   "peak; merge GB/s",

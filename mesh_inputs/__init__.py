@@ -94,6 +94,17 @@ WORKLOADS = {
         note="1M tokens striped over 256 partitions, 16x16 tile "
              "Q24..39 x KV16..31"),
 }
+# Forward launches of equal-length items: one Q partition of 4096 rows
+# against 16 KV partitions, non-causal, Hq query heads on Hq/4 KV heads, so
+# 16 Q blocks x Hq heads = 64, 128, 256 or 512 workgroups of 1024 KV blocks
+# each keep a quarter, half, all or twice all of the 256 compute units busy.
+for _hq in (4, 8, 16, 32):
+    _name = f"items-{16 * _hq}"
+    WORKLOADS[_name] = TileConfig(
+        _name, 64, 4096, [0], list(range(16, 32)), _hq, _hq // 4, 128, False,
+        seed=11, note=f"{16 * _hq} equal items: Q partition 0 x KV 16..31, "
+                      f"{_hq} q heads / {_hq // 4} kv heads, non-causal")
+del _hq, _name
 
 
 def make_qkv(cfg: TileConfig):
