@@ -34,6 +34,10 @@ resident in HBM (all bf16, head_dim 128):
                    compute units busy: the same work per compute unit at
                    different chip load, which separates the kernel's
                    efficiency in clock cycles from the clock the chip holds.
+  bwd_items64 .. bwd_items256  (not in the default step) the backward on
+                   64, 128 or 256 dK/dV items of equal length (a quarter,
+                   half or all of the compute units for the dK/dV kernel),
+                   for the same comparison.
 
 `value` is the headline tile's forward TFLOP/s: algorithmic FLOPs
 (4 * d * Hq * visible (query, key) pairs) divided by the forward call's mean
@@ -61,8 +65,11 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 DEFAULT_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal", "merge", "bwd",
                 "chunks")
 ITEM_LEGS = ("fwd_items64", "fwd_items128", "fwd_items256", "fwd_items512")
+BWD_ITEM_LEGS = ("bwd_items64", "bwd_items128", "bwd_items256")
 FWD_LEGS = ("fwd", "fwd_causal64k", "fwd_mesh1m_causal") + ITEM_LEGS
-ALL_LEGS = DEFAULT_LEGS + ("bwd_striped", "bwd_gqa") + ITEM_LEGS
+BWD_LEGS = ("bwd", "bwd_striped", "bwd_gqa") + BWD_ITEM_LEGS
+ALL_LEGS = (DEFAULT_LEGS + ("bwd_striped", "bwd_gqa") + ITEM_LEGS +
+            BWD_ITEM_LEGS)
 
 
 def log(msg):
@@ -264,6 +271,12 @@ def main():
     for name in ITEM_LEGS:
         if name in legs:
             tiles[name] = Tile(ma, WORKLOADS[f"items-{name[9:]}"], dev)
+    for name in BWD_ITEM_LEGS:
+        if name in legs:
+            t = Tile(ma, WORKLOADS[f"bwd-items-{name[9:]}"], dev,
+                     with_bwd=True)
+            t.fwd(ma)
+            tiles[name] = t
     if "bwd" in legs:
         # The backward workload is the backward of the causal 64K tile: same
         # inputs (seed 1), dO from seed 4, O and LSE from its forward, which
@@ -328,7 +341,7 @@ def main():
         for name in legs:
             if name in FWD_LEGS:
                 leg(name, ev, lambda: tiles[name].fwd(ma))
-            elif name in ("bwd", "bwd_striped", "bwd_gqa"):
+            elif name in BWD_LEGS:
                 leg(name, ev, lambda: tiles[name].bwd(ma))
             elif name == "merge":
                 leg(name, ev, lambda: ma.mesh_attn_lse_merge(
@@ -442,7 +455,7 @@ def main():
                              "bytes": mbytes,
                              "shape": f"k={mk} x {mrows} rows x {mh} heads x "
                                       f"{md}, bf16 in/out"}
-    for name in ("bwd", "bwd_striped", "bwd_gqa"):
+    for name in BWD_LEGS:
         if name not in legs:
             continue
         t = tiles[name]
@@ -471,6 +484,8 @@ def main():
                  "bwd_gqa": "tile_bwd(mesh1m-nc-gqa)",
                  "chunks": f"{args.chunks} chunk_fwd({head_cfg.name})"}
     step_desc.update({n: f"tile_fwd(items-{n[9:]})" for n in ITEM_LEGS})
+    step_desc.update({n: f"tile_bwd(bwd-items-{n[9:]})"
+                      for n in BWD_ITEM_LEGS})
     line = {
         "metric": "tile attention fwd TFLOP/s on 1 MI355X + % of bf16 MFMA "
                   "peak; merge GB/s",

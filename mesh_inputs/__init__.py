@@ -104,7 +104,18 @@ for _hq in (4, 8, 16, 32):
         _name, 64, 4096, [0], list(range(16, 32)), _hq, _hq // 4, 128, False,
         seed=11, note=f"{16 * _hq} equal items: Q partition 0 x KV 16..31, "
                       f"{_hq} q heads / {_hq // 4} kv heads, non-causal")
-del _hq, _name
+# Backward launches of equal-length dK/dV items: 16 Q partitions of 4096
+# rows against 2, 4 or 8 KV partitions, non-causal, 4 query heads on one KV
+# head, so 64, 128 or 256 dK/dV workgroups of 128 keys, each over all 65536
+# query rows of the group's 4 heads.
+for _nkv in (2, 4, 8):
+    _name = f"bwd-items-{32 * _nkv}"
+    WORKLOADS[_name] = TileConfig(
+        _name, 64, 4096, list(range(16)), list(range(32, 32 + _nkv)), 4, 1,
+        128, False, seed=12, grad_seed=13,
+        note=f"{32 * _nkv} equal dK/dV items: Q 0..15 x KV 32..{31 + _nkv}, "
+             f"4 q heads / 1 kv head, non-causal; dO from seed 13")
+del _hq, _nkv, _name
 
 
 def make_qkv(cfg: TileConfig):
